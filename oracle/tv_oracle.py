@@ -1,0 +1,369 @@
+"""Float64 CPU oracle of the tree-verify path.
+
+TEST INFRASTRUCTURE ONLY: used by the test suite, the smoke check and the
+benchmark's CPU-baseline leg; never by the library.  Shares no code with the
+GPU path.
+
+What it computes, with the paper passage each step follows:
+
+* ``build_tree_mask``: the verification plan of the draft tree (Sec. 4.1,
+  verify preprocess turns the tree into candidate chains; Sec. 3.1: a candidate sees the
+  accepted context plus the ancestors on its own branch).  Bit ``j`` of
+  ``anc[i]`` is set iff node ``j`` is ``i`` or an ancestor of ``i``.
+* ``branch_compress``: each branch compresses its own not-yet-full block,
+  never mixing sibling branches (Sec. 4.1, chains compressed independently
+  after branching; Sec. 4.2, isolated compression state per chain kept in a
+  scratch pad).
+* ``verify_attention``: branch-aware causal verification over the compressed
+  history (Sec. 3.1, Sec. 4.1 target verify; Sec. 2.2 multi-resolution
+  compressed context).  A node attends to CSA entries chosen by the indexer
+  top-k, all HCA entries, and the raw sliding window, restricted to entries
+  whose tokens lie on its own root path.
+* ``commit_accepted_path``: refresh of token history, window KV and the
+  compressed states along the accepted path only (Sec. 3.2 and Sec. 4.2,
+  accepted-path refresh; rejected branches leave no trace).
+
+The paper cites DeepSeek-V4 for the CSA/HCA arithmetic without restating it.
+The reading taken here (kept identical on the GPU side):
+
+* compression of a ratio-r block is softmax-gated pooling: gate logit
+  ``z_q = g_r . u_q`` over the full raw row, ``alpha = softmax(z)`` over the r
+  tokens of the block, entry ``sum_q alpha_q u_q``; the CSA entry keeps every
+  channel (latent row plus indexer key), the HCA entry the latent row only;
+* the CSA indexer score of entry s for a query node is
+  ``sum_h w[h] * relu(q_idx[h] . k_s)``; the node keeps the top-k candidates
+  by (score descending, logical index ascending);
+* one softmax runs over the selected CSA entries, all visible HCA entries and
+  the raw window of the last ``window`` positions up to and including the
+  node; keys are ``row[:d_k]``, values ``row[v_off:v_off+d_v]``;
+* an entry is visible from the query at its closing position onward.
+
+All arithmetic is float64.  Inputs are bfloat16 bit patterns, widened
+exactly; a value the cache stores (a compressed entry) is rounded to
+bfloat16, round-to-nearest-even, before anything reads it.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = 0, 1, 2, 3, 4
+
+
+# --------------------------------------------------------------------------
+# bfloat16 conversions
+# --------------------------------------------------------------------------
+def bf16_to_f64(bits) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) to float64, exactly."""
+    b = np.asarray(bits, dtype=np.uint16)
+    with np.errstate(invalid="ignore"):  # NaN patterns stay NaN
+        return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def f64_to_bf16(x) -> np.ndarray:
+    """float64 to bfloat16 bits, one rounding, to nearest with ties to even.
+
+    bfloat16 keeps 8 significant bits and the float32 exponent range, so the
+    spacing of representable values around ``x = f * 2**E`` (0.5 <= f < 1) is
+    ``2**(E-8)``, never finer than the subnormal spacing ``2**-133``.
+    ``x / spacing`` is an exact power-of-two scaling, ``rint`` rounds it half to
+    even, and the product is exactly representable in float32.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("non-finite value")
+    _, e = np.frexp(x)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    y = np.rint(x / spacing) * spacing
+    big = np.abs(y) >= 2.0 ** 128
+    y = np.where(big, np.copysign(np.inf, x), y)
+    return (y.astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def round_bf16(x) -> np.ndarray:
+    return bf16_to_f64(f64_to_bf16(x))
+
+
+# --------------------------------------------------------------------------
+# verification plan
+# --------------------------------------------------------------------------
+def build_tree_mask(parents):
+    """Ancestor masks, depths and row status of a batch of draft trees.
+
+    ``parents[b][i]`` is the parent of node i; node 0 is the root (parent -1)
+    and every parent precedes its child.  A row breaking this gets status
+    BAD_PARENT and zero masks and depths.
+    """
+    parents = np.asarray(parents, dtype=np.int64)
+    B, D = parents.shape
+    anc = np.zeros((B, D), dtype=np.uint64)
+    depth = np.zeros((B, D), dtype=np.int32)
+    status = np.zeros(B, dtype=np.int32)
+    for b in range(B):
+        p = parents[b]
+        ok = p[0] == -1 and all(0 <= p[i] < i for i in range(1, D))
+        if not ok:
+            status[b] = ROW_BAD_PARENT
+            continue
+        m = [0] * D
+        m[0] = 1
+        for i in range(1, D):
+            depth[b, i] = depth[b, p[i]] + 1
+            m[i] = m[p[i]] | (1 << i)
+        anc[b] = np.array(m, dtype=np.uint64)
+    return anc, depth, status
+
+
+def node_path(anc_row, depth_row, i):
+    """Nodes on the root path of node i, ordered by depth (root first)."""
+    bits = int(anc_row[i])
+    path = [j for j in range(len(depth_row)) if (bits >> j) & 1]
+    path.sort(key=lambda j: int(depth_row[j]))
+    return path
+
+
+def _len_ok(L, dims):
+    return 0 <= L <= dims["max_len"]
+
+
+def _token(wl, b, path, L, q):
+    """Raw row (float64, all d_u channels) at absolute position q on a branch."""
+    if q < L:
+        return bf16_to_f64(wl.ring[b, q & (wl.dims["ring_cap"] - 1)])
+    return bf16_to_f64(wl.tree_u[b, path[q - L]])
+
+
+def compress_block(tokens, gate):
+    """Softmax-gated pooling of the r raw rows of one block (float64)."""
+    z = tokens @ gate
+    a = np.exp(z - z.max())
+    a /= a.sum()
+    return a @ tokens
+
+
+# --------------------------------------------------------------------------
+# per-branch compression into scratch
+# --------------------------------------------------------------------------
+def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None):
+    """Compressed entries closed by each node along its own branch.
+
+    Node i at position ``p = L + depth[i]`` closes a ratio-r block when
+    ``(p + 1) % r == 0``; the block covers positions ``p-r+1 .. p`` of the
+    sequence ``committed || root path of i``.  CSA entries (all d_u channels)
+    go to ``scr_c4[b][i]``, HCA entries (the d_row latent channels) to
+    ``scr_c128[b][i]``; other slots are left as given.  Returns the scratch
+    arrays, the written-slot masks and the updated row status.
+    """
+    d = wl.dims
+    B, D = d["B"], d["D"]
+    d_row, d_u = d["d_row"], d["d_row"] + d["d_idx"]
+    if scr_c4 is None:
+        scr_c4 = np.zeros((B, D, d_u), dtype=np.uint16)
+    if scr_c128 is None:
+        scr_c128 = np.zeros((B, D, d_row), dtype=np.uint16)
+    scr_c4, scr_c128 = scr_c4.copy(), scr_c128.copy()
+    status = np.array(row_status, dtype=np.int32).copy()
+    w4 = np.zeros((B, D), dtype=bool)
+    w128 = np.zeros((B, D), dtype=bool)
+    g = bf16_to_f64(wl.gate_w)
+    for b in range(B):
+        if status[b] != ROW_OK:
+            continue
+        L = int(wl.lens[b])
+        if not _len_ok(L, d):
+            status[b] = ROW_BAD_LEN
+            continue
+        for i in range(D):
+            path = node_path(anc[b], depth[b], i)
+            p = L + int(depth[b, i])
+            for ri, r in enumerate((d["ratio_csa"], d["ratio_hca"])):
+                if (p + 1) % r:
+                    continue
+                toks = np.stack([_token(wl, b, path, L, q) for q in range(p - r + 1, p + 1)])
+                e = compress_block(toks, g[ri])
+                if ri == 0:
+                    scr_c4[b, i] = f64_to_bf16(e)
+                    w4[b, i] = True
+                else:
+                    scr_c128[b, i] = f64_to_bf16(e[:d_row])
+                    w128[b, i] = True
+    return scr_c4, scr_c128, w4, w128, status
+
+
+# --------------------------------------------------------------------------
+# verify attention
+# --------------------------------------------------------------------------
+class _RowCache:
+    """Float64 views of one row's committed state, widened once."""
+
+    def __init__(self, wl, b):
+        d = wl.dims
+        self.L = L = int(wl.lens[b])
+        self.n4 = L // d["ratio_csa"]
+        self.n128 = L // d["ratio_hca"]
+        base4, base128 = int(wl.c4_base[b]), int(wl.c128_base[b])
+        self.k4 = bf16_to_f64(wl.c4_idx[base4:base4 + self.n4])
+        self.c4_bits = wl.c4[base4:base4 + self.n4]
+        self.c128 = bf16_to_f64(wl.c128[base128:base128 + self.n128])
+
+
+def indexer_scores(keys, q_idx, w_idx):
+    """S(s) = sum_h w[h] * relu(q_idx[h] . k_s) for every key row (float64)."""
+    return np.maximum(keys @ q_idx.T, 0.0) @ w_idx
+
+
+def verify_node(wl, b, i, anc, depth, scr_c4, scr_c128, rc=None):
+    """Output of node i of row b: the definition written out for one query.
+
+    Returns a dict with ``out`` [H][d_v], ``lse`` [H], ``sel`` (selected CSA
+    logical indices, ascending), ``scores`` (logical index -> indexer score of
+    every candidate) and ``n_keys`` (size of the attended key set).
+    """
+    d = wl.dims
+    r4, r128, W, k = d["ratio_csa"], d["ratio_hca"], d["window"], d["topk"]
+    d_row, d_k, v_off, d_v = d["d_row"], d["d_k"], d["v_off"], d["d_v"]
+    if rc is None:
+        rc = _RowCache(wl, b)
+    L = rc.L
+    path = node_path(anc[b], depth[b], i)
+    p = L + int(depth[b, i])
+    pos = {j: L + int(depth[b, j]) for j in path}
+
+    # CSA candidates: committed entries, then entries closed on this branch.
+    cand_idx = list(range(rc.n4))
+    cand_keys = [rc.k4]
+    scratch_rows = {}
+    for j in path:
+        if (pos[j] + 1) % r4 == 0:
+            s = (pos[j] + 1) // r4 - 1
+            cand_idx.append(s)
+            cand_keys.append(bf16_to_f64(scr_c4[b, j, d_row:])[None, :])
+            scratch_rows[s] = bf16_to_f64(scr_c4[b, j, :d_row])
+    cand_idx = np.asarray(cand_idx, dtype=np.int64)
+    keys = np.concatenate(cand_keys, axis=0) if len(cand_idx) else np.zeros((0, d["d_idx"]))
+    S = indexer_scores(keys, bf16_to_f64(wl.q_idx[b, i]), bf16_to_f64(wl.w_idx[b, i]))
+    order = np.lexsort((cand_idx, -S))  # score descending, then index ascending
+    chosen = np.sort(cand_idx[order[:min(k, len(cand_idx))]])
+
+    rows = []
+    for s in chosen:
+        rows.append(scratch_rows[s] if s >= rc.n4 else bf16_to_f64(rc.c4_bits[s]))
+    rows.extend(rc.c128)
+    for j in path:
+        if (pos[j] + 1) % r128 == 0:
+            rows.append(bf16_to_f64(scr_c128[b, j]))
+    for qpos in range(max(0, p - W + 1), p + 1):
+        rows.append(_token(wl, b, path, L, qpos)[:d_row])
+    R = np.stack(rows) if rows else np.zeros((0, d_row))
+
+    Q = bf16_to_f64(wl.q[b, i])                       # [H][d_k]
+    scale = float(np.float32(d["scale"]))
+    logits = scale * (Q @ R[:, :d_k].T)               # [H][n_keys]
+    m = logits.max(axis=1, keepdims=True)
+    e = np.exp(logits - m)
+    s = e.sum(axis=1, keepdims=True)
+    out = (e / s) @ R[:, v_off:v_off + d_v]
+    lse = (m + np.log(s))[:, 0]
+    return dict(out=out, lse=lse, sel=chosen, scores=dict(zip(cand_idx.tolist(), S.tolist())),
+                n_keys=R.shape[0])
+
+
+def verify_attention(wl, anc, depth, scr_c4, scr_c128, row_status, nodes=None):
+    """Verify outputs for every node of every valid row (or for ``nodes``).
+
+    Returns ``out`` float64 [B][D][H][d_v], ``lse`` [B][D][H], ``sel`` int32
+    [B][D][topk] (ascending, -1 padded), ``status`` and per-node details.
+    Rows with a nonzero status are skipped (outputs left NaN, sel -1).
+    """
+    d = wl.dims
+    B, D, H = d["B"], d["D"], d["H"]
+    out = np.full((B, D, H, d["d_v"]), np.nan)
+    lse = np.full((B, D, H), np.nan)
+    sel = np.full((B, D, d["topk"]), -1, dtype=np.int32)
+    status = np.array(row_status, dtype=np.int32).copy()
+    detail = {}
+    want = nodes if nodes is not None else [(b, i) for b in range(B) for i in range(D)]
+    rcs = {}
+    for b, i in want:
+        if status[b] != ROW_OK:
+            continue
+        if not _len_ok(int(wl.lens[b]), d):
+            status[b] = ROW_BAD_LEN
+            continue
+        if b not in rcs:
+            rcs.clear()
+            rcs[b] = _RowCache(wl, b)
+        r = verify_node(wl, b, i, anc, depth, scr_c4, scr_c128, rcs[b])
+        out[b, i], lse[b, i] = r["out"], r["lse"]
+        sel[b, i, :len(r["sel"])] = r["sel"]
+        detail[(b, i)] = r
+    return out, lse, sel, status, detail
+
+
+# --------------------------------------------------------------------------
+# accepted-path commit
+# --------------------------------------------------------------------------
+def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_status,
+                         accept_nodes=None, accept_len=None):
+    """Refresh the committed state along the accepted path of every valid row.
+
+    The accepted path is the root path of ``accepted_last[b]`` (a = depth + 1
+    tokens).  Its raw rows enter the ring at positions L..L+a-1, each of its
+    nodes that closed a block writes its scratch entry to the pool at the
+    entry's logical index, and ``len`` becomes L + a.  A row whose new entries
+    would not fit its pool capacity gets status CAPACITY and is left intact.
+    Returns a dict of new arrays (inputs are not modified).
+    """
+    d = wl.dims
+    B, D = d["B"], d["D"]
+    r4, r128, cap = d["ratio_csa"], d["ratio_hca"], d["ring_cap"]
+    d_row = d["d_row"]
+    ring, c4, c4_idx, c128 = wl.ring.copy(), wl.c4.copy(), wl.c4_idx.copy(), wl.c128.copy()
+    lens = wl.lens.copy()
+    status = np.array(row_status, dtype=np.int32).copy()
+    an = np.full((B, D), -1, dtype=np.int32) if accept_nodes is None else accept_nodes.copy()
+    al = np.zeros(B, dtype=np.int32) if accept_len is None else accept_len.copy()
+    for b in range(B):
+        if status[b] != ROW_OK:
+            continue
+        L = int(lens[b])
+        if not _len_ok(L, d):
+            status[b] = ROW_BAD_LEN
+            continue
+        last = int(accepted_last[b])
+        if not 0 <= last < D:
+            status[b] = ROW_BAD_ACCEPT
+            continue
+        path = node_path(anc[b], depth[b], last)
+        writes4, writes128 = [], []
+        for j in path:
+            p = L + int(depth[b, j])
+            if (p + 1) % r4 == 0:
+                writes4.append(((p + 1) // r4 - 1, j))
+            if (p + 1) % r128 == 0:
+                writes128.append(((p + 1) // r128 - 1, j))
+        if any(s >= wl.c4_cap[b] for s, _ in writes4) or any(s >= wl.c128_cap[b] for s, _ in writes128):
+            status[b] = ROW_CAPACITY
+            continue
+        for t, j in enumerate(path):
+            ring[b, (L + t) & (cap - 1)] = wl.tree_u[b, j]
+        for s, j in writes4:
+            c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
+            c4_idx[wl.c4_base[b] + s] = scr_c4[b, j, d_row:]
+        for s, j in writes128:
+            c128[wl.c128_base[b] + s] = scr_c128[b, j]
+        lens[b] = L + len(path)
+        an[b] = -1
+        an[b, :len(path)] = path
+        al[b] = len(path)
+    return dict(ring=ring, c4=c4, c4_idx=c4_idx, c128=c128, lens=lens, status=status,
+                accept_nodes=an, accept_len=al)
+
+
+def run_round(wl, nodes=None):
+    """All four steps on one workload; returns every intermediate."""
+    anc, depth, st = build_tree_mask(wl.parents)
+    scr4, scr128, w4, w128, st = branch_compress(wl, anc, depth, st)
+    out, lse, sel, st_v, det = verify_attention(wl, anc, depth, scr4, scr128, st, nodes)
+    com = commit_accepted_path(wl, anc, depth, scr4, scr128, wl.accepted_last, st_v)
+    return dict(anc=anc, depth=depth, scr_c4=scr4, scr_c128=scr128, w4=w4, w128=w128,
+                out=out, lse=lse, sel=sel, status_verify=st_v, detail=det, commit=com)
