@@ -1,0 +1,204 @@
+/*
+ * tv.h - tree-structured speculative verification over CSA/HCA compressed
+ * attention, for one MI355X (gfx950) GPU.
+ *
+ * The library implements the target-verify step of tree speculation on a model
+ * whose history is compressed online along the sequence (the paper's Sec. 3
+ * "Challenges" and Sec. 4 "Our Approach"):
+ *
+ *   tv_build_tree_mask       verify preprocess: draft tree -> per-node ancestor
+ *                            bitmask and depth (Sec. 4.1; device-side metadata,
+ *                            Sec. 4.3)
+ *   tv_branch_compress       each node compresses the block it closes along its
+ *                            own root path into a scratch slot, never mixing
+ *                            branches (Sec. 4.1, Sec. 4.2)
+ *   tv_verify_attention      branch-aware causal verification: every node
+ *                            attends to the committed compressed history plus
+ *                            its own ancestors only (Sec. 3.1, Sec. 4.1)
+ *   tv_commit_accepted_path  accepted-path refresh of token window, CSA and HCA
+ *                            state; rejected branches leave no trace (Sec. 3.2,
+ *                            Sec. 4.2)
+ *
+ * Reading of the compressed-attention arithmetic (the paper cites DeepSeek-V4
+ * for it): a ratio-r entry pools the r raw rows of a block with softmax
+ * weights of the gate logits g_r . u; the CSA (ratio_csa) entry keeps every
+ * channel of the raw row (latent row, then indexer key), the HCA (ratio_hca)
+ * entry the latent row.  A node scores every visible CSA entry with
+ * sum_h w[h] * relu(q_idx[h] . key), keeps the topk best (score descending,
+ * then logical index ascending), and runs one softmax over those entries,
+ * every visible HCA entry and the raw window of the last `window` positions
+ * up to and including itself.  Keys are row[0:d_k], values row[v_off:v_off+d_v].
+ *
+ * Conventions shared by every call
+ *   - Every pointer is device memory owned by the caller.  The library never
+ *     allocates device memory and keeps no state between calls besides device
+ *     properties and the optional profiling records.
+ *   - Calls enqueue work on `stream` and return without synchronising the
+ *     host.  Issue them in the order mask -> compress -> verify -> commit.
+ *   - Floating-point buffers hold bfloat16 bit patterns (uint16_t) unless
+ *     stated otherwise; arithmetic is float32 on the device.
+ *   - A row is the draft tree of one sequence.  Node 0 is the root; node i has
+ *     parent parents[i] < i.  The committed length of row b is len[b] = L; the
+ *     root stands at position L and node i at L + depth[i].
+ *   - Host-checkable problems return a tv_status other than TV_OK and launch
+ *     nothing.  Data problems found on the device are written to
+ *     row_status[b] (first error wins); a row whose status is not TV_ROW_OK is
+ *     skipped by every later call and its outputs and cache are left as they
+ *     were.
+ */
+#ifndef TV_H
+#define TV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TV_OK = 0,
+  TV_ERR_INVALID_ARG = 1, /* null pointer, bad size or inconsistent dims */
+  TV_ERR_UNSUPPORTED = 2, /* valid dims the library has no kernel for */
+  TV_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  TV_ERR_LAUNCH = 4,      /* a HIP call failed while enqueuing work */
+  TV_ERR_DEVICE = 5       /* no current HIP device, or it is not gfx950 */
+} tv_status;
+
+/* Per-row data errors written to row_status[b]. */
+enum {
+  TV_ROW_OK = 0,
+  TV_ROW_BAD_PARENT = 1, /* parents[b][0] != -1 or parents[b][i] outside [0, i) */
+  TV_ROW_BAD_ACCEPT = 2, /* accepted_last[b] outside [0, D) */
+  TV_ROW_CAPACITY = 3,   /* a committed entry would land beyond c4_cap/c128_cap */
+  TV_ROW_BAD_LEN = 4     /* len[b] < 0 or len[b] > max_len */
+};
+
+/* Sizes of one verify round.  Supported head shapes:
+ *   H=64, d_row=576, d_k=576, v_off=0,   d_v=512  (shared MLA latent row)
+ *   H=8,  d_row=256, d_k=128, v_off=128, d_v=128  (one KV head, row = K|V)
+ * with d_idx = 64 and H_idx a power of two <= 64. */
+typedef struct {
+  int32_t B;         /* rows (sequences), 1..4096 */
+  int32_t D;         /* tree nodes per row including the root, 1..64 */
+  int32_t H;         /* query heads sharing the single KV row */
+  int32_t d_row;     /* width of a latent KV row (compressed entries, window keys) */
+  int32_t d_k;       /* key channels row[0:d_k] */
+  int32_t v_off;     /* value channels row[v_off:v_off+d_v] */
+  int32_t d_v;
+  int32_t d_idx;     /* indexer key width; a raw token row has d_u = d_row + d_idx channels */
+  int32_t H_idx;     /* indexer heads */
+  int32_t ratio_csa; /* CSA compression ratio (4) */
+  int32_t ratio_hca; /* HCA compression ratio (128) */
+  int32_t window;    /* raw sliding window in positions, the query included (128) */
+  int32_t topk;      /* CSA entries kept per node, >= 1 */
+  int32_t ring_cap;  /* raw-token ring slots per row: power of two >= max(window, ratio_csa, ratio_hca) */
+  int32_t max_len;   /* bound on every len[b]; sizes launches and the verify workspace */
+  float scale;       /* logit scale, normally 1/sqrt(d_k) */
+} tv_dims;
+
+/* Committed (persistent) state of every row.  Only tv_commit_accepted_path
+ * writes it; compress and verify only read it (Sec. 4.2: speculative branch
+ * state never touches the persistent cache before acceptance). */
+typedef struct {
+  uint16_t *ring;   /* [B][ring_cap][d_row + d_idx]: raw row of position q in slot q & (ring_cap-1) */
+  uint16_t *c4;     /* [*][d_row]: CSA entry s of row b at c4[c4_base[b] + s], s < len/ratio_csa */
+  uint16_t *c4_idx; /* [*][d_idx]: indexer key of the same CSA entry */
+  uint16_t *c128;   /* [*][d_row]: HCA entry s of row b at c128[c128_base[b] + s] */
+  const int64_t *c4_base;   /* [B] first pool slot of each row */
+  const int32_t *c4_cap;    /* [B] pool slots owned by each row */
+  const int64_t *c128_base; /* [B] */
+  const int32_t *c128_cap;  /* [B] */
+  int32_t *len;             /* [B] committed tokens L of each row */
+} tv_cache;
+
+/* Verify preprocess (Sec. 4.1): for every row, validate the parent array and
+ * build per node the ancestor bitmask (bit j set iff node j is i or an ancestor
+ * of i; bit i set, bit 0 set) and depth (root 0).
+ *   parents    int32 [B][D], read
+ *   anc        uint64 [B][D], written (0 for a bad row)
+ *   depth      int32 [B][D], written (0 for a bad row)
+ *   row_status int32 [B], written: TV_ROW_OK or TV_ROW_BAD_PARENT (resets the row) */
+tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64_t *anc,
+                             int32_t *depth, int32_t *row_status, hipStream_t stream);
+
+/* Per-branch compression into scratch (Sec. 4.1, Sec. 4.2).  Node i at
+ * position p = L + depth[i] closes a ratio-r block when (p + 1) % r == 0; the
+ * block is positions p-r+1..p of "committed tokens, then the root path of i"
+ * (committed tokens from the ring, path tokens from tree_u).  Its CSA entry
+ * (d_row + d_idx channels) goes to scr_c4[b][i], its HCA entry (d_row
+ * channels) to scr_c128[b][i]; slots of nodes that close nothing are not
+ * written.
+ *   tree_u   [B][D][d_row + d_idx] raw rows of the draft tokens, read
+ *   gate_w   [2][d_row + d_idx] gate vectors for ratio_csa then ratio_hca, read
+ *   row_status in/out: a row with len outside [0, max_len] becomes TV_ROW_BAD_LEN */
+tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                             const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w,
+                             uint16_t *scr_c4, uint16_t *scr_c128, int32_t *row_status,
+                             hipStream_t stream);
+
+/* Bytes of device workspace tv_verify_attention needs for these dims (the
+ * largest row is bounded by dims->max_len).  0 on invalid dims. */
+size_t tv_verify_workspace_bytes(const tv_dims *dims);
+
+/* Branch-aware verify attention (Sec. 3.1, Sec. 4.1).  For node i of row b:
+ *   CSA candidates: committed entries 0..L/ratio_csa-1 and the scratch entries
+ *     closed by i and its ancestors (logical index (p_j+1)/ratio_csa - 1);
+ *   HCA keys: committed entries and the scratch entries closed on the path;
+ *   window keys: raw rows of positions max(0, p_i-window+1)..p_i (committed
+ *     ones from the ring, path ones from tree_u).
+ *   q        [B][D][H][d_k], q_idx [B][D][H_idx][d_idx], w_idx [B][D][H_idx], read
+ *   out      [B][D][H][d_v] bfloat16, written
+ *   lse      float32 [B][D][H] natural-log sum of exp(logits), written if not NULL
+ *   sel      int32 [B][D][topk] chosen CSA logical indices ascending, -1 padded,
+ *            written if not NULL
+ *   workspace  device scratch of at least tv_verify_workspace_bytes(dims),
+ *            contents on entry ignored
+ * Reads the cache only.  Rows with nonzero status are skipped. */
+tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                              const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                              const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                              const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel,
+                              int32_t *row_status, void *workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* Accepted-path refresh (Sec. 3.2, Sec. 4.2).  The accepted path is the root
+ * path of accepted_last[b], a = depth + 1 nodes.  Writes the raw rows of the
+ * path into ring slots of positions L..L+a-1, the scratch entry of every path
+ * node that closed a block into the pools at its logical index, len[b] = L + a,
+ * accept_nodes[b][0:a] = path (root first, -1 after it) and accept_len[b] = a.
+ * A row that fails a check (accept index, pool capacity) is left untouched and
+ * gets the row status.
+ *   parents, depth, anc: as produced by tv_build_tree_mask (read)
+ *   accepted_last int32 [B], accept_nodes int32 [B][D], accept_len int32 [B] */
+tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const uint16_t *tree_u,
+                                  const uint64_t *anc, const int32_t *depth,
+                                  const uint16_t *scr_c4, const uint16_t *scr_c128,
+                                  const int32_t *accepted_last, int32_t *accept_nodes,
+                                  int32_t *accept_len, int32_t *row_status, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char *tv_status_string(int status);
+
+/* Optional kernel timing.  While enabled, every kernel the library launches is
+ * bracketed by HIP events recorded on the caller's stream (at most `capacity`
+ * launches are recorded; later ones run untimed).  tv_profile_read waits for
+ * the recorded events and returns, per kernel name, the launch count and the
+ * summed duration in milliseconds; it resets the records. */
+typedef struct {
+  char name[32];
+  int32_t launches;
+  double total_ms;
+} tv_kernel_time;
+
+tv_status tv_profile_enable(int32_t capacity);
+tv_status tv_profile_disable(void);
+tv_status tv_profile_read(tv_kernel_time *out, int32_t max_entries, int32_t *n_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TV_H */

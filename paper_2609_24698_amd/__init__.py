@@ -1,0 +1,24 @@
+"""Tree-structured speculative verification over CSA/HCA compressed attention on MI355X.
+
+The compute path is the gfx950 HIP library ``lib/libtv.so`` (C ABI in
+``include/tv.h``); this package is its Python binding.
+"""
+from .binding import (  # noqa: F401
+    EXPORTED,
+    DeviceRound,
+    TvCache,
+    TvDims,
+    TvError,
+    lib,
+    make_cache,
+    make_dims,
+    status_string,
+    tv_branch_compress,
+    tv_build_tree_mask,
+    tv_commit_accepted_path,
+    tv_profile_disable,
+    tv_profile_enable,
+    tv_profile_read,
+    tv_verify_attention,
+    tv_verify_workspace_bytes,
+)

@@ -1,0 +1,254 @@
+"""ctypes binding of ``libtv.so``: the C ABI of ``include/tv.h`` with torch tensors.
+
+Argument marshalling only.  Every step runs in the library's HIP kernels; there
+is no Python or CPU fallback, and loading fails loudly when the library has
+not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "lib", "libtv.so")
+
+TV_OK, TV_ERR_INVALID_ARG, TV_ERR_UNSUPPORTED, TV_ERR_WORKSPACE, TV_ERR_LAUNCH, TV_ERR_DEVICE = range(6)
+ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = range(5)
+
+EXPORTED = (
+    "tv_build_tree_mask", "tv_branch_compress", "tv_verify_workspace_bytes", "tv_verify_attention",
+    "tv_commit_accepted_path", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
+)
+
+
+class TvError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        super().__init__(f"{where}: {status_string(code)} ({code})")
+        self.code = code
+
+
+class TvDims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "B", "D", "H", "d_row", "d_k", "v_off", "d_v", "d_idx", "H_idx", "ratio_csa", "ratio_hca", "window",
+        "topk", "ring_cap", "max_len")] + [("scale", ctypes.c_float)]
+
+
+class TvCache(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "ring", "c4", "c4_idx", "c128", "c4_base", "c4_cap", "c128_base", "c128_cap", "len")]
+
+
+class TvKernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2609_24698_amd._build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        dp = ctypes.POINTER(TvDims)
+        cp = ctypes.POINTER(TvCache)
+        L.tv_build_tree_mask.argtypes = [dp, vp, vp, vp, vp, vp]
+        L.tv_branch_compress.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tv_verify_workspace_bytes.argtypes = [dp]
+        L.tv_verify_workspace_bytes.restype = sz
+        L.tv_verify_attention.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.tv_commit_accepted_path.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tv_status_string.argtypes = [ctypes.c_int]
+        L.tv_status_string.restype = ctypes.c_char_p
+        L.tv_profile_enable.argtypes = [i32]
+        L.tv_profile_read.argtypes = [ctypes.POINTER(TvKernelTime), i32, ctypes.POINTER(i32)]
+        for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_commit_accepted_path",
+                     "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().tv_status_string(int(code)).decode()
+
+
+def _check(code: int, where: str) -> None:
+    if code != TV_OK:
+        raise TvError(code, where)
+
+
+def make_dims(d: dict) -> TvDims:
+    return TvDims(**{f: (float(d[f]) if f == "scale" else int(d[f])) for f, _ in TvDims._fields_})
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"expected {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def make_cache(ring, c4, c4_idx, c128, c4_base, c4_cap, c128_base, c128_cap, lens) -> TvCache:
+    """Cache struct over device tensors (bf16/int16 pools, int64 bases, int32 caps and lengths)."""
+    return TvCache(_ptr(ring), _ptr(c4), _ptr(c4_idx), _ptr(c128), _ptr(c4_base, torch.int64),
+                   _ptr(c4_cap, torch.int32), _ptr(c128_base, torch.int64), _ptr(c128_cap, torch.int32),
+                   _ptr(lens, torch.int32))
+
+
+def tv_build_tree_mask(dims: TvDims, parents, anc, depth, row_status, stream=None) -> None:
+    _check(lib().tv_build_tree_mask(ctypes.byref(dims), _ptr(parents, torch.int32), _ptr(anc, torch.int64),
+                                    _ptr(depth, torch.int32), _ptr(row_status, torch.int32), _stream(stream)),
+           "tv_build_tree_mask")
+
+
+def tv_branch_compress(dims: TvDims, cache: TvCache, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status,
+                       stream=None) -> None:
+    _check(lib().tv_branch_compress(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u), _ptr(anc, torch.int64),
+                                    _ptr(depth, torch.int32), _ptr(gate_w), _ptr(scr_c4), _ptr(scr_c128),
+                                    _ptr(row_status, torch.int32), _stream(stream)),
+           "tv_branch_compress")
+
+
+def tv_verify_workspace_bytes(dims: TvDims) -> int:
+    return int(lib().tv_verify_workspace_bytes(ctypes.byref(dims)))
+
+
+def tv_verify_attention(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out,
+                        lse, sel, row_status, workspace, stream=None) -> None:
+    _check(lib().tv_verify_attention(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u), _ptr(anc, torch.int64),
+                                     _ptr(depth, torch.int32), _ptr(scr_c4), _ptr(scr_c128), _ptr(q), _ptr(q_idx),
+                                     _ptr(w_idx), _ptr(out), _ptr(lse, torch.float32), _ptr(sel, torch.int32),
+                                     _ptr(row_status, torch.int32), _ptr(workspace), workspace.numel() *
+                                     workspace.element_size(), _stream(stream)),
+           "tv_verify_attention")
+
+
+def tv_commit_accepted_path(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
+                            accept_nodes, accept_len, row_status, stream=None) -> None:
+    _check(lib().tv_commit_accepted_path(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u),
+                                         _ptr(anc, torch.int64), _ptr(depth, torch.int32), _ptr(scr_c4),
+                                         _ptr(scr_c128), _ptr(accepted_last, torch.int32),
+                                         _ptr(accept_nodes, torch.int32), _ptr(accept_len, torch.int32),
+                                         _ptr(row_status, torch.int32), _stream(stream)),
+           "tv_commit_accepted_path")
+
+
+def tv_profile_enable(capacity: int) -> None:
+    _check(lib().tv_profile_enable(int(capacity)), "tv_profile_enable")
+
+
+def tv_profile_disable() -> None:
+    _check(lib().tv_profile_disable(), "tv_profile_disable")
+
+
+def tv_profile_read(max_entries: int = 32) -> dict:
+    arr = (TvKernelTime * max_entries)()
+    n = ctypes.c_int32(0)
+    _check(lib().tv_profile_read(arr, max_entries, ctypes.byref(n)), "tv_profile_read")
+    return {arr[k].name.decode(): (int(arr[k].launches), float(arr[k].total_ms)) for k in range(n.value)}
+
+
+# ---------------------------------------------------------------------------
+# Device-resident round state: uploads host arrays and owns every buffer the
+# four calls read or write.
+# ---------------------------------------------------------------------------
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(device)
+    if a.dtype == np.uint64:
+        return torch.from_numpy(a.view(np.int64)).to(device)
+    return torch.from_numpy(a).to(device)
+
+
+class DeviceRound:
+    """Device buffers of one verify round built from host arrays.
+
+    ``src`` needs the attributes dims, lens, parents, accepted_last, ring, c4,
+    c4_idx, c128, c4_base, c4_cap, c128_base, c128_cap, tree_u, q, q_idx,
+    w_idx, gate_w (numpy, bfloat16 data as uint16).
+    """
+
+    def __init__(self, src, device="cuda:0", poison_outputs: bool = True):
+        dev = torch.device(device)
+        d = dict(src.dims)
+        self.host_dims = d
+        self.dims = make_dims(d)
+        B, D, H = d["B"], d["D"], d["H"]
+        d_u = d["d_row"] + d["d_idx"]
+        T = {}
+        for k in ("parents", "accepted_last", "ring", "c4", "c4_idx", "c128", "c4_base", "c4_cap", "c128_base",
+                  "c128_cap", "tree_u", "q", "q_idx", "w_idx", "gate_w"):
+            T[k] = _dev(getattr(src, k), dev)
+        T["len"] = _dev(src.lens.astype(np.int32), dev)
+        fill = -1 if poison_outputs else 0  # 0xFFFF bf16 is NaN: unwritten outputs show up
+        T["anc"] = torch.full((B, D), fill, dtype=torch.int64, device=dev)
+        T["depth"] = torch.full((B, D), fill, dtype=torch.int32, device=dev)
+        T["row_status"] = torch.full((B,), fill, dtype=torch.int32, device=dev)
+        T["scr_c4"] = torch.full((B, D, d_u), fill, dtype=torch.int16, device=dev)
+        T["scr_c128"] = torch.full((B, D, d["d_row"]), fill, dtype=torch.int16, device=dev)
+        T["out"] = torch.full((B, D, H, d["d_v"]), fill, dtype=torch.int16, device=dev)
+        T["lse"] = torch.full((B, D, H), float("nan"), dtype=torch.float32, device=dev)
+        T["sel"] = torch.full((B, D, d["topk"]), -2, dtype=torch.int32, device=dev)
+        T["accept_nodes"] = torch.full((B, D), -2, dtype=torch.int32, device=dev)
+        T["accept_len"] = torch.full((B,), -2, dtype=torch.int32, device=dev)
+        ws = tv_verify_workspace_bytes(self.dims)
+        if ws == 0:
+            raise TvError(TV_ERR_INVALID_ARG, "tv_verify_workspace_bytes")
+        T["workspace"] = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.t = T
+        self.cache = make_cache(T["ring"], T["c4"], T["c4_idx"], T["c128"], T["c4_base"], T["c4_cap"],
+                                T["c128_base"], T["c128_cap"], T["len"])
+
+    def mask(self, stream=None):
+        t = self.t
+        tv_build_tree_mask(self.dims, t["parents"], t["anc"], t["depth"], t["row_status"], stream)
+
+    def compress(self, stream=None):
+        t = self.t
+        tv_branch_compress(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["gate_w"], t["scr_c4"],
+                           t["scr_c128"], t["row_status"], stream)
+
+    def verify(self, stream=None, with_sel: bool = True, with_lse: bool = True):
+        t = self.t
+        tv_verify_attention(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"], t["scr_c128"],
+                            t["q"], t["q_idx"], t["w_idx"], t["out"], t["lse"] if with_lse else None,
+                            t["sel"] if with_sel else None, t["row_status"], t["workspace"], stream)
+
+    def commit(self, stream=None):
+        t = self.t
+        tv_commit_accepted_path(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"],
+                                t["scr_c128"], t["accepted_last"], t["accept_nodes"], t["accept_len"],
+                                t["row_status"], stream)
+
+    def round(self, stream=None):
+        self.mask(stream)
+        self.compress(stream)
+        self.verify(stream)
+        self.commit(stream)
+
+    def host(self, name: str) -> np.ndarray:
+        x = self.t[name].cpu().numpy()
+        if x.dtype == np.int16:
+            return x.view(np.uint16)
+        if name == "anc":
+            return x.view(np.uint64)
+        return x

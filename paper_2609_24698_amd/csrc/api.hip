@@ -1,0 +1,275 @@
+// C ABI of the tree-verify library: argument checks, workspace layout,
+// launch sequencing and optional kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "tv_internal.h"
+
+namespace tv {
+
+static bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+static bool shape_supported(const tv_dims &d) {
+  const bool mla = d.H == 64 && d.d_row == 576 && d.d_k == 576 && d.v_off == 0 && d.d_v == 512;
+  const bool mha = d.H == 8 && d.d_row == 256 && d.d_k == 128 && d.v_off == 128 && d.d_v == 128;
+  return (mla || mha) && d.d_idx == 64 && pow2(d.H_idx) && d.H_idx <= 64;
+}
+
+// Dimension checks shared by every entry point.
+static tv_status check_dims(const tv_dims *dp) {
+  if (!dp) return TV_ERR_INVALID_ARG;
+  const tv_dims &d = *dp;
+  if (d.B < 1 || d.D < 1 || d.D > 64) return TV_ERR_INVALID_ARG;
+  if (d.H < 1 || d.d_row < 1 || d.d_k < 1 || d.d_v < 1 || d.v_off < 0 || d.d_idx < 1 || d.H_idx < 1)
+    return TV_ERR_INVALID_ARG;
+  if (d.d_k > d.d_row || d.v_off + d.d_v > d.d_row || d.d_row % 8 || d.d_idx % 8) return TV_ERR_INVALID_ARG;
+  if (d.ratio_csa < 1 || d.ratio_hca < 1 || d.ratio_csa > 1024 || d.ratio_hca > 1024) return TV_ERR_INVALID_ARG;
+  if (d.window < 1 || d.topk < 1) return TV_ERR_INVALID_ARG;
+  if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window, d.ratio_csa, d.ratio_hca})) return TV_ERR_INVALID_ARG;
+  if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
+  if (!std::isfinite(d.scale)) return TV_ERR_INVALID_ARG;
+  if (d.B > 4096 || !shape_supported(d)) return TV_ERR_UNSUPPORTED;
+  return TV_OK;
+}
+
+static bool cache_complete(const tv_cache *c) {
+  return c && c->ring && c->c4 && c->c4_idx && c->c128 && c->c4_base && c->c4_cap && c->c128_base &&
+         c->c128_cap && c->len;
+}
+
+// The library only runs on gfx950; the answer is cached per device.
+static tv_status check_device() {
+  static std::mutex mu;
+  static std::vector<int> verdict;  // -1 unknown, 0 bad, 1 good
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TV_ERR_DEVICE;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)verdict.size() <= dev) verdict.resize(dev + 1, -1);
+  if (verdict[dev] < 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return TV_ERR_DEVICE;
+    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
+  }
+  return verdict[dev] == 1 ? TV_OK : TV_ERR_DEVICE;
+}
+
+SplitPlan split_plan(const tv_dims &d) {
+  SplitPlan p;
+  const int64_t mk = (int64_t)d.topk + d.max_len / d.ratio_hca + d.D + d.window;
+  p.max_keys = (int32_t)mk;
+  const int64_t nodes = (int64_t)d.B * d.D;
+  int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (512 + nodes - 1) / nodes));
+  splits = (int)std::min<int64_t>(splits, (mk + 31) / 32);
+  int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
+  p.chunk = (int32_t)chunk;
+  p.splits = (int32_t)((mk + chunk - 1) / chunk);
+  return p;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+WsLayout ws_layout(const tv_dims &d) {
+  WsLayout w;
+  w.plan = split_plan(d);
+  const int64_t nodes = (int64_t)d.B * d.D;
+  w.score_stride = (int32_t)((d.max_len / d.ratio_csa + 63) / 64 * 64);
+  size_t off = 0;
+  w.scores = off;
+  off = align256(off + sizeof(float) * nodes * std::max(w.score_stride, 1));
+  w.sel = off;
+  off = align256(off + sizeof(int32_t) * nodes * d.topk);
+  w.part_o = off;
+  if (w.plan.splits > 1) off = align256(off + sizeof(float) * nodes * w.plan.splits * d.H * d.d_v);
+  w.part_ml = off;
+  if (w.plan.splits > 1) off = align256(off + sizeof(float) * 2 * nodes * w.plan.splits * d.H);
+  w.total = off;
+  return w;
+}
+
+// ---- kernel timing -------------------------------------------------------
+namespace {
+struct ProfRec {
+  const char *name;
+  hipEvent_t start, stop;
+};
+struct Prof {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<ProfRec> recs;
+  size_t cap = 0;
+  bool pending = false;
+} g_prof;
+}  // namespace
+
+void prof_before(const char *name, hipStream_t s) {
+  if (!g_prof.on) return;
+  if (g_prof.recs.size() >= g_prof.cap) return;
+  ProfRec r{name, g_prof.pool[2 * g_prof.recs.size()], g_prof.pool[2 * g_prof.recs.size() + 1]};
+  hipEventRecord(r.start, s);
+  g_prof.recs.push_back(r);
+  g_prof.pending = true;
+}
+
+void prof_after(hipStream_t s) {
+  if (!g_prof.on || !g_prof.pending) return;
+  hipEventRecord(g_prof.recs.back().stop, s);
+  g_prof.pending = false;
+}
+
+static CacheView view(const tv_cache &c) {
+  return CacheView{c.ring, c.c4, c.c4_idx, c.c128, c.c4_base, c.c128_base, c.c4_cap, c.c128_cap, c.len};
+}
+
+#define TV_LAUNCH(name, call)            \
+  do {                                   \
+    prof_before(name, stream);           \
+    hipError_t e_ = (call);              \
+    prof_after(stream);                  \
+    if (e_ != hipSuccess) return TV_ERR_LAUNCH; \
+  } while (0)
+
+}  // namespace tv
+
+using namespace tv;
+
+extern "C" {
+
+const char *tv_status_string(int s) {
+  switch (s) {
+    case TV_OK: return "ok";
+    case TV_ERR_INVALID_ARG: return "invalid argument";
+    case TV_ERR_UNSUPPORTED: return "unsupported dimensions";
+    case TV_ERR_WORKSPACE: return "workspace missing or too small";
+    case TV_ERR_LAUNCH: return "kernel launch failed";
+    case TV_ERR_DEVICE: return "no gfx950 device";
+    default: return "unknown status";
+  }
+}
+
+tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64_t *anc, int32_t *depth,
+                             int32_t *row_status, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!parents || !anc || !depth || !row_status) return TV_ERR_INVALID_ARG;
+  if ((st = check_device()) != TV_OK) return st;
+  TV_LAUNCH("tree_mask", launch_mask(*dims, parents, anc, depth, row_status, stream));
+  return TV_OK;
+}
+
+tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                             const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4,
+                             uint16_t *scr_c128, int32_t *row_status, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if ((st = check_device()) != TV_OK) return st;
+  TV_LAUNCH("branch_compress", launch_compress(*dims, view(*cache), tree_u, anc, depth, gate_w, scr_c4, scr_c128,
+                                               row_status, stream));
+  return TV_OK;
+}
+
+size_t tv_verify_workspace_bytes(const tv_dims *dims) {
+  if (check_dims(dims) != TV_OK) return 0;
+  return ws_layout(*dims).total;
+}
+
+tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                              const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                              const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                              const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel, int32_t *row_status,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
+      !out || !row_status)
+    return TV_ERR_INVALID_ARG;
+  const WsLayout w = ws_layout(*dims);
+  if (!workspace || workspace_bytes < w.total) return TV_ERR_WORKSPACE;
+  if ((st = check_device()) != TV_OK) return st;
+  const tv_dims &d = *dims;
+  char *ws = static_cast<char *>(workspace);
+  float *scores = reinterpret_cast<float *>(ws + w.scores);
+  int32_t *selp = sel ? sel : reinterpret_cast<int32_t *>(ws + w.sel);
+  float *part_o = reinterpret_cast<float *>(ws + w.part_o);
+  float *part_ml = reinterpret_cast<float *>(ws + w.part_ml);
+  const CacheView cv = view(*cache);
+  TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
+  TV_LAUNCH("topk_select", launch_topk(d, cv, anc, depth, scr_c4, q_idx, w_idx, scores, w.score_stride, selp,
+                                       row_status, stream));
+  TV_LAUNCH("verify_attn", launch_attn(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q, selp, row_status, w.plan,
+                                       part_o, part_ml, out, lse, stream));
+  if (w.plan.splits > 1)
+    TV_LAUNCH("attn_combine", launch_combine(d, cv, anc, depth, selp, row_status, w.plan, part_o, part_ml, out, lse,
+                                             stream));
+  return TV_OK;
+}
+
+tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const uint16_t *tree_u, const uint64_t *anc,
+                                  const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
+                                  const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
+                                  int32_t *row_status, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
+      !accept_nodes || !accept_len || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if ((st = check_device()) != TV_OK) return st;
+  TV_LAUNCH("commit_path", launch_commit(*dims, *cache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
+                                         accept_nodes, accept_len, row_status, stream));
+  return TV_OK;
+}
+
+tv_status tv_profile_enable(int32_t capacity) {
+  if (capacity < 1 || capacity > (1 << 20)) return TV_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  for (hipEvent_t e : g_prof.pool) hipEventDestroy(e);
+  g_prof.pool.assign(2 * (size_t)capacity, nullptr);
+  for (auto &e : g_prof.pool)
+    if (hipEventCreate(&e) != hipSuccess) return TV_ERR_DEVICE;
+  g_prof.recs.clear();
+  g_prof.recs.reserve(capacity);
+  g_prof.cap = capacity;
+  g_prof.on = true;
+  return TV_OK;
+}
+
+tv_status tv_profile_disable(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  return TV_OK;
+}
+
+tv_status tv_profile_read(tv_kernel_time *out, int32_t max_entries, int32_t *n_entries) {
+  if (!out || !n_entries || max_entries < 1) return TV_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  std::vector<tv_kernel_time> acc;
+  for (const ProfRec &r : g_prof.recs) {
+    if (hipEventSynchronize(r.stop) != hipSuccess) return TV_ERR_DEVICE;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) return TV_ERR_DEVICE;
+    auto it = std::find_if(acc.begin(), acc.end(), [&](const tv_kernel_time &k) { return std::strcmp(k.name, r.name) == 0; });
+    if (it == acc.end()) {
+      tv_kernel_time k{};
+      std::strncpy(k.name, r.name, sizeof(k.name) - 1);
+      acc.push_back(k);
+      it = acc.end() - 1;
+    }
+    it->launches += 1;
+    it->total_ms += ms;
+  }
+  g_prof.recs.clear();
+  const int n = (int)std::min<size_t>(acc.size(), (size_t)max_entries);
+  for (int k = 0; k < n; ++k) out[k] = acc[k];
+  *n_entries = n;
+  return TV_OK;
+}
+
+}  // extern "C"

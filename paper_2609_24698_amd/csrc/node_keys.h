@@ -1,0 +1,85 @@
+// The key set one tree node attends to, enumerated without materialising it.
+//
+// Node i of row b stands at position p = L + depth[i].  Its keys, in order:
+//   [0, nsel)            CSA entries chosen by the indexer top-k (sel list,
+//                        ascending logical index; an index >= L/ratio_csa is
+//                        an entry closed on i's own root path, held in scratch)
+//   [.., + n128)         committed HCA entries
+//   [.., + s128)         HCA entries closed on the root path (scratch)
+//   [.., + nwin_c)       committed raw rows of positions win_lo..L-1
+//   [.., + npath)        raw rows of the path nodes at positions max(L, win_lo)..p
+// so a node sees the committed history and its own ancestors only
+// (branch-aware causal visibility, Sec. 3.1).
+#pragma once
+
+#include "tv_common.h"
+
+namespace tv {
+
+struct NodeKeys {
+  int32_t L, n4, n128, nsel, s128, nwin_c, npath, n_keys;
+  int64_t p, win_lo;
+};
+
+// Fills path[d] (ancestor at depth d, d <= depth of i) and hca_node[t] (t-th
+// path node closing an HCA block) in shared memory; must be called by every
+// thread of the block (contains barriers).
+__device__ inline NodeKeys node_keys(const tv_dims &d, int32_t L, int b, int i, const uint64_t *anc,
+                                     const int32_t *depth, int32_t *path, int32_t *hca_node, int32_t *cnt) {
+  const int tid = threadIdx.x;
+  const uint64_t m = anc[(int64_t)b * d.D + i];
+  if (tid == 0) { cnt[0] = 0; cnt[1] = 0; }
+  __syncthreads();
+  if (tid < d.D && ((m >> tid) & 1ull)) {
+    const int dj = depth[(int64_t)b * d.D + tid];
+    path[dj] = tid;
+    const int64_t pj = (int64_t)L + dj;
+    if ((pj + 1) % d.ratio_csa == 0) atomicAdd(&cnt[0], 1);
+    if ((pj + 1) % d.ratio_hca == 0) hca_node[(pj + 1) / d.ratio_hca - 1 - L / d.ratio_hca] = tid;
+    if ((pj + 1) % d.ratio_hca == 0) atomicAdd(&cnt[1], 1);
+  }
+  __syncthreads();
+  NodeKeys k;
+  k.L = L;
+  k.p = (int64_t)L + depth[(int64_t)b * d.D + i];
+  k.n4 = L / d.ratio_csa;
+  k.n128 = L / d.ratio_hca;
+  const int cand = k.n4 + cnt[0];
+  k.nsel = cand < d.topk ? cand : d.topk;
+  k.s128 = cnt[1];
+  const int64_t lo = k.p - d.window + 1;
+  k.win_lo = lo > 0 ? lo : 0;
+  k.nwin_c = (int32_t)(k.win_lo < L ? L - k.win_lo : 0);
+  const int64_t pstart = k.win_lo > L ? k.win_lo : L;
+  k.npath = (int32_t)(k.p - pstart + 1);
+  k.n_keys = k.nsel + k.n128 + k.s128 + k.nwin_c + k.npath;
+  return k;
+}
+
+// Pointer to the latent row (first d_row channels) of key t of the node.
+__device__ inline const uint16_t *key_row(const tv_dims &d, const NodeKeys &k, int b, int t,
+                                          const int32_t *sel_node, const int32_t *path, const int32_t *hca_node,
+                                          const uint16_t *ring, const uint16_t *c4, const int64_t c4_base,
+                                          const uint16_t *c128, const int64_t c128_base, const uint16_t *scr_c4,
+                                          const uint16_t *scr_c128, const uint16_t *tree_u) {
+  const int d_u = d.d_row + d.d_idx;
+  if (t < k.nsel) {
+    int s = sel_node[t];
+    if (s < 0) s = 0;  // defensive: a selection list is never shorter than nsel
+    if (s < k.n4) return c4 + (c4_base + s) * d.d_row;
+    int64_t dd = (int64_t)(s + 1) * d.ratio_csa - 1 - k.L;
+    if (dd < 0 || dd > k.p - k.L) dd = 0;  // defensive: stay on the node's own path
+    return scr_c4 + ((int64_t)b * d.D + path[dd]) * d_u;
+  }
+  t -= k.nsel;
+  if (t < k.n128) return c128 + (c128_base + t) * d.d_row;
+  t -= k.n128;
+  if (t < k.s128) return scr_c128 + ((int64_t)b * d.D + hca_node[t]) * d.d_row;
+  t -= k.s128;
+  if (t < k.nwin_c) return ring_row(ring, b, d.ring_cap, d_u, k.win_lo + t);
+  t -= k.nwin_c;
+  const int64_t q = (k.win_lo > k.L ? k.win_lo : k.L) + t;
+  return tree_u + ((int64_t)b * d.D + path[q - k.L]) * d_u;
+}
+
+}  // namespace tv

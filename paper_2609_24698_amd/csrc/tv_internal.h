@@ -1,0 +1,67 @@
+// Host-side plumbing shared by the API and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/tv.h"
+
+namespace tv {
+
+// Device-resident pointers of one verify call, passed to kernels by value.
+struct CacheView {
+  const uint16_t *ring, *c4, *c4_idx, *c128;
+  const int64_t *c4_base, *c128_base;
+  const int32_t *c4_cap, *c128_cap;
+  const int32_t *len;
+};
+
+// How the verify attention splits a node's keys across workgroups.
+struct SplitPlan {
+  int32_t max_keys;   // upper bound of any node's key count
+  int32_t chunk;      // keys per split (multiple of the key tile)
+  int32_t splits;     // splits per node
+};
+
+// Byte offsets of the verify workspace regions.
+struct WsLayout {
+  size_t scores;      // float [B*D][score_stride]
+  size_t sel;         // int32 [B*D][topk], used when the caller passes no sel
+  size_t part_o;      // float [B*D][splits][H][d_v]
+  size_t part_ml;     // float2 [B*D][splits][H] (running max in log2 units, sum)
+  size_t total;
+  int32_t score_stride;
+  SplitPlan plan;
+};
+
+SplitPlan split_plan(const tv_dims &d);
+WsLayout ws_layout(const tv_dims &d);
+
+hipError_t launch_mask(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
+                       int32_t *row_status, hipStream_t s);
+hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
+                           const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4, uint16_t *scr_c128,
+                           int32_t *row_status, hipStream_t s);
+hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
+                        const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s);
+hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
+                       const uint16_t *scr_c4, const uint16_t *q_idx, const uint16_t *w_idx, const float *scores,
+                       int32_t score_stride, int32_t *sel, int32_t *row_status, hipStream_t s);
+hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
+                       const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
+                       const int32_t *sel, const int32_t *row_status, const SplitPlan &plan, float *part_o,
+                       float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+hipError_t launch_combine(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
+                          const int32_t *sel, const int32_t *row_status, const SplitPlan &plan,
+                          const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
+                         const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
+                         const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
+                         int32_t *row_status, hipStream_t s);
+
+// Kernel timing hooks (no-ops unless profiling is enabled).
+void prof_before(const char *name, hipStream_t s);
+void prof_after(hipStream_t s);
+
+}  // namespace tv

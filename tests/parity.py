@@ -1,0 +1,94 @@
+"""Comparison helpers for GPU-vs-oracle parity tests.
+
+Tolerances: ancestor masks, depths, accepted-path lists, commit layout and
+integer status are bit-exact.  Attention outputs and compressed entries are
+bfloat16 and must be within max-abs 2e-2 and mean-abs 2e-3 of the oracle's
+float64 value rounded to bfloat16.  CSA selections must be identical except
+where the oracle's scores at the selection boundary are within 1e-5 relative
+of each other (near ties that float32 scoring may order differently).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import tv_oracle as O
+
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+TIE_REL = 1e-5
+LSE_ABS = 2e-3
+
+
+def bf16_err(gpu_bits: np.ndarray, ref_f64: np.ndarray):
+    g = O.bf16_to_f64(gpu_bits)
+    r = O.round_bf16(ref_f64)
+    assert np.all(np.isfinite(g)), "GPU output holds NaN/inf (unwritten or corrupted)"
+    e = np.abs(g - r)
+    return float(e.max()) if e.size else 0.0, float(e.mean()) if e.size else 0.0
+
+
+def assert_bf16_close(gpu_bits, ref_f64, what: str):
+    mx, mean = bf16_err(gpu_bits, ref_f64)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max-abs {mx:.3e} mean-abs {mean:.3e}"
+    return mx, mean
+
+
+def selection_matches(gpu_sel: np.ndarray, ref_detail: dict, k: int):
+    """True if identical; 'tie' if they differ only within near-ties; False otherwise."""
+    ref = np.asarray(ref_detail["sel"])
+    g = gpu_sel[gpu_sel >= 0]
+    if len(g) == len(ref) and np.array_equal(np.sort(g), ref):
+        return True
+    if len(g) != len(ref):
+        return False
+    scores = ref_detail["scores"]
+    vals = sorted(scores.values(), reverse=True)
+    if len(vals) <= k:
+        return False
+    kth = vals[k - 1]
+    diff = set(g.tolist()) ^ set(ref.tolist())
+    tol = TIE_REL * max(abs(kth), 1e-30)
+    if all(s in scores and abs(scores[s] - kth) <= tol for s in diff):
+        return "tie"
+    return False
+
+
+def compare_verify(gpu_out, gpu_lse, gpu_sel, ref, nodes, dims, n4_rows=None):
+    """Compare verify outputs node by node; returns stats.
+
+    ``n4_rows`` (committed CSA entries per row) is given when the GPU verified
+    against its own scratch entries rather than the oracle's: those may differ
+    from the oracle's in the last bfloat16 bit, which may move a scratch
+    candidate across the selection boundary; such nodes are counted, not failed.
+    """
+    k = dims["topk"]
+    ties = scratch = 0
+    worst = 0.0
+    sums = 0.0
+    count = 0
+    for (b, i) in nodes:
+        det = ref["detail"][(b, i)]
+        m = selection_matches(gpu_sel[b, i], det, k)
+        if m is False and n4_rows is not None:
+            g = gpu_sel[b, i][gpu_sel[b, i] >= 0]
+            diff = set(g.tolist()) ^ set(np.asarray(det["sel"]).tolist())
+            if any(s >= n4_rows[b] for s in diff):
+                m = "scratch"
+        assert m is not False, f"selection mismatch at row {b} node {i}"
+        if m == "tie":
+            ties += 1
+            continue
+        if m == "scratch":
+            scratch += 1
+            continue
+        mx, mean = bf16_err(gpu_out[b, i], det["out"])
+        assert mx <= MAX_ABS, f"out row {b} node {i}: max-abs {mx:.3e}"
+        worst = max(worst, mx)
+        sums += mean
+        count += 1
+        if gpu_lse is not None:
+            le = np.abs(gpu_lse[b, i].astype(np.float64) - det["lse"]).max()
+            assert le <= LSE_ABS, f"lse row {b} node {i}: {le:.3e}"
+    mean_all = sums / max(count, 1)
+    assert mean_all <= MEAN_ABS, f"out mean-abs {mean_all:.3e}"
+    return dict(nodes=count, ties=ties, scratch_sel=scratch, max_abs=worst, mean_abs=mean_all)

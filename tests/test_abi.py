@@ -1,0 +1,82 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects bad
+arguments on the host before touching a GPU (these calls run without one)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_24698_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "tv.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(tv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.lib()
+    names = _declared()
+    assert "tv_verify_attention" in names and len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(binding.EXPORTED)
+
+
+def _dims(**over):
+    d = dict(B=2, D=5, H=8, d_row=256, d_k=128, v_off=128, d_v=128, d_idx=64, H_idx=8, ratio_csa=4, ratio_hca=128,
+             window=128, topk=64, ring_cap=256, max_len=4096, scale=0.088)
+    d.update(over)
+    return binding.make_dims(d)
+
+
+BAD = [dict(B=0), dict(D=0), dict(D=65), dict(topk=0), dict(window=0), dict(ring_cap=200), dict(ring_cap=64),
+       dict(ratio_csa=0), dict(max_len=-1), dict(v_off=200), dict(scale=float("inf"))]
+
+
+@pytest.mark.parametrize("over", BAD, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_bad_dims_rejected_without_gpu(over):
+    lib = binding.lib()
+    d = _dims(**over)
+    assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_verify_workspace_bytes(ctypes.byref(d)) == 0
+
+
+def test_unsupported_shapes():
+    lib = binding.lib()
+    for over in (dict(H=16), dict(d_idx=32), dict(H_idx=3), dict(B=5000)):
+        d = _dims(**over)
+        assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == binding.TV_ERR_UNSUPPORTED
+
+
+def test_null_pointers_rejected_without_gpu():
+    lib = binding.lib()
+    d = _dims()
+    assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == binding.TV_ERR_INVALID_ARG
+    cache = binding.TvCache()
+    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([None] * 8)) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_commit_accepted_path(ctypes.byref(d), ctypes.byref(cache), *([None] * 10)) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_verify_attention(ctypes.byref(d), ctypes.byref(cache), *([None] * 13), 0, None) == \
+        binding.TV_ERR_INVALID_ARG
+
+
+def test_workspace_size_grows_with_max_len():
+    lib = binding.lib()
+    a = lib.tv_verify_workspace_bytes(ctypes.byref(_dims(max_len=1024)))
+    b = lib.tv_verify_workspace_bytes(ctypes.byref(_dims(max_len=65536)))
+    assert 0 < a < b
+
+
+def test_status_strings():
+    assert binding.status_string(0) == "ok"
+    assert "workspace" in binding.status_string(3)
+    assert binding.status_string(99) == "unknown status"
+
+
+def test_profile_capacity_checked_without_gpu():
+    lib = binding.lib()
+    assert lib.tv_profile_enable(0) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_profile_read(None, 4, None) == binding.TV_ERR_INVALID_ARG
