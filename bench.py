@@ -1,0 +1,256 @@
+"""Benchmark of one verify round per step on one MI355X.
+
+A step is the whole hot path over one batch: tree mask, per-branch
+compression, verify attention and accepted-path commit, for B rows of D-node
+draft trees.  Every step commits its accepted path, so the committed context
+grows by the accepted length (at most D tokens per row per step) like a
+decoding loop would.  Inputs are synthetic and already resident in HBM.
+
+Prints one JSON line: verified tree tokens per second (B * D per step), the
+roofline of the dominant kernel (verify attention, HBM bound, algorithmic
+bytes per launch over its mean duration from HIP events recorded on the
+launch stream during the timed steps) and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified tree tokens/sec at B=64,D=8,16K ctx; % of MI355X peak HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+DOMINANT = "verify_attn"
+KERNEL_SOURCES = {"verify_attn": ["attn.hip", "node_keys.h", "tv_common.h"]}
+
+WORKLOADS = {
+    "C3": "B=64 rows, committed length log-uniform in [1024, 65536] (partially filled 128-token tail), "
+          "D=8 random draft trees, 64 query heads over a 576-wide latent (values 512), CSA ratio 4 with top-k 512, "
+          "HCA ratio 128, window 128",
+    "C1": "B=8 rows, L=8192, D=6 random trees, 64 heads over a 576-wide latent, CSA top-k 512",
+    "C2": "B=32 rows, L=32768, D=8 random trees, 64 heads over a 576-wide latent, CSA top-k 512",
+    "C4": "B=1 row, L=1048576, D=8 random tree, 64 heads over a 576-wide latent, CSA top-k 2048",
+    "C0": "B=1 row, L=2048, tree [-1,0,0,1,1], 8 heads over one 128-wide KV head, CSA top-k 64",
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2609_24698_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def attention_bytes(dims, lens, sel, depth, anc):
+    """Algorithmic HBM bytes of one verify-attention launch.
+
+    Queries, outputs (bf16) and lse; the selection lists; the union over the
+    row's nodes of the CSA rows they select (each row once); every HCA entry a
+    node of the row sees; the committed window rows of the row (the root's
+    window is the widest); the row's draft-token rows.
+    """
+    B, D, H = dims["B"], dims["D"], dims["H"]
+    row = dims["d_row"] * 2
+    total = B * D * H * (dims["d_k"] * 2 + dims["d_v"] * 2 + 4)
+    total += B * D * dims["topk"] * 4
+    for b in range(B):
+        L = int(lens[b])
+        s = sel[b]
+        total += len(np.unique(s[s >= 0])) * row
+        total += (L // dims["ratio_hca"]) * row
+        hca_closers = {j for j in range(D) if (L + int(depth[b, j]) + 1) % dims["ratio_hca"] == 0}
+        total += len(hca_closers) * row
+        total += min(L, dims["window"] - 1) * row
+        total += D * row
+    return total
+
+
+def step_bytes(dims, lens, sel, depth, anc):
+    """Algorithmic bytes of the whole step: attention plus the indexer keys and queries."""
+    n4 = sum(int(L) // dims["ratio_csa"] for L in lens)
+    b = attention_bytes(dims, lens, sel, depth, anc)
+    b += n4 * dims["d_idx"] * 2
+    b += dims["B"] * dims["D"] * dims["H_idx"] * (dims["d_idx"] * 2 + 2)
+    return b
+
+
+def _first_rows(wl, n):
+    """The same workload restricted to its first n rows (pools stay shared)."""
+    import dataclasses
+
+    dims = dict(wl.dims)
+    dims["B"] = n
+    cut = {k: getattr(wl, k)[:n] for k in ("lens", "parents", "accepted_last", "ring", "c4_base", "c4_cap",
+                                           "c128_base", "c128_cap", "tree_u", "q", "q_idx", "w_idx")}
+    return dataclasses.replace(wl, dims=dims, **cut)
+
+
+def cpu_baseline(wl, budget_s: float):
+    """The CPU oracle (all four steps) on the first rows of the same workload.
+
+    One row is timed first to size the sample so that the timed run takes
+    about ``budget_s`` seconds; the sample is then timed as a whole.
+    """
+    from oracle import tv_oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    t0 = time.perf_counter()
+    O.run_round(_first_rows(wl, 1))
+    t1 = time.perf_counter() - t0
+    rows = int(max(1, min(wl.B, budget_s // max(t1, 1e-3))))
+    sub = _first_rows(wl, rows)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:  # whole passes over the sample until the budget is spent
+        O.run_round(sub)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or rows < wl.B:
+            break
+    return dict(value=round(reps * rows * wl.D / dt, 2), unit="tokens/s", cores=int(cores), kind="oracle",
+                sample=f"all four steps for the first {rows} of {wl.B} rows ({rows * wl.D} tree nodes, mean "
+                       f"length {float(sub.lens.mean()):.0f}) of the same workload, {reps} pass(es), float64 "
+                       f"numpy oracle, {dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="C3", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check of the first step")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2609_24698_amd import DeviceRound, binding
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    K, W = args.steps, args.warmup
+    D_cfg = synth.CONFIGS[args.config]["D"]
+    grow = (K + W + 2) * D_cfg
+    wl = synth.make_workload(args.config, seed=args.seed, max_len_margin=grow,
+                             extra_c4=grow // 4 + 8, extra_c128=grow // 128 + 4)
+    dims = wl.dims
+    print(f"[bench] {args.config}: B={wl.B} D={wl.D} mean L={wl.lens.mean():.0f} "
+          f"input {wl.nbytes() / 1e6:.0f} MB", file=sys.stderr, flush=True)
+    r = DeviceRound(wl, "cuda:0", poison_outputs=False)
+
+    # first step, checked against the oracle on sampled nodes
+    r.mask()
+    r.compress()
+    r.verify()
+    torch.cuda.synchronize()
+    sel0 = r.host("sel")
+    depth0, anc0 = r.host("depth"), r.host("anc")
+    lens0 = r.host("len").copy()
+    if not args.no_check:
+        from oracle import tv_oracle as O
+
+        rng = np.random.default_rng(0)
+        bs = sorted(set(rng.integers(0, wl.B, size=min(4, wl.B)).tolist()))
+        nodes = [(b, i) for b in bs for i in range(wl.D)]
+        anc, depth, st = O.build_tree_mask(wl.parents)
+        scr4, scr128, w4, w128, st = O.branch_compress(wl, anc, depth, st)
+        out, lse, sel, st, det = O.verify_attention(wl, anc, depth, scr4, scr128, st, nodes)
+        g = O.bf16_to_f64(r.host("out"))
+        worst = 0.0
+        for (b, i) in nodes:
+            if np.array_equal(sel0[b, i][sel0[b, i] >= 0], det[(b, i)]["sel"]):
+                worst = max(worst, float(np.abs(g[b, i] - O.round_bf16(out[b, i])).max()))
+        assert worst <= 2e-2, f"first-step check failed: max-abs {worst}"
+        print(f"[bench] first step matches the oracle on {len(nodes)} nodes (max-abs {worst:.2e})",
+              file=sys.stderr, flush=True)
+    r.commit()
+    for _ in range(W):
+        r.round()
+    torch.cuda.synchronize()
+
+    binding.tv_profile_enable(8 * K + 16)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(K):
+        r.round()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern = binding.tv_profile_read()
+    binding.tv_profile_disable()
+    gpu_ms = ev0.elapsed_time(ev1)
+    status = r.host("row_status")
+    assert np.all(status == 0), f"rows left the workload: {np.unique(status)}"
+
+    ms_per_step = gpu_ms / K
+    tokens = wl.B * wl.D
+    value = tokens * K / (gpu_ms / 1e3)
+    launches, tot = kern[DOMINANT]
+    avg_ms = tot / launches
+    a_bytes = attention_bytes(dims, lens0, sel0, depth0, anc0)
+    achieved = a_bytes / (avg_ms / 1e3) / 1e9
+    s_bytes = step_bytes(dims, lens0, sel0, depth0, anc0)
+
+    traffic = None
+    pmc_file = os.path.join(ROOT, "profiles", f"{DOMINANT}_{args.config}_pmc.json")
+    if os.path.exists(pmc_file):
+        with open(pmc_file) as f:
+            pmc = json.load(f)
+        if pmc.get("source_hash") == kernel_source_hash(DOMINANT):
+            traffic = pmc.get("hbm_bytes_per_launch")
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "B": wl.B, "D": wl.D,
+                   "mean_len": round(float(wl.lens.mean()), 1), "seed": wl.seed,
+                   "step_algorithmic_bytes": int(s_bytes),
+                   "step_hbm_frac": round(s_bytes / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "kernels_ms_per_step": {k: round(v[1] / K, 4) for k, v in kern.items()}},
+        "roofline": {"bound": "hbm", "kernel": DOMINANT, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": int(a_bytes), "avg_launch_ms": round(avg_ms, 5)},
+    }
+    print(f"[bench] {K} steps in {gpu_ms:.2f} ms GPU ({wall * 1e3:.2f} ms wall); per-kernel ms/step: "
+          + ", ".join(f"{k} {v[1] / K:.4f}" for k, v in kern.items()), file=sys.stderr, flush=True)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
