@@ -66,6 +66,7 @@ SplitPlan split_plan(const tv_dims &d) {
   const int64_t nodes = (int64_t)d.B * d.D;
   int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (512 + nodes - 1) / nodes));
   splits = (int)std::min<int64_t>(splits, (mk + 31) / 32);
+  splits = (int)std::max<int64_t>(splits, (mk + 1535) / 1536);  // the attention kernel's pointer table bound
   int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
   p.chunk = (int32_t)chunk;
   p.splits = (int32_t)((mk + chunk - 1) / chunk);

@@ -1,15 +1,24 @@
 // Branch-aware verify attention over CSA / HCA / window keys.
 //
-// One workgroup (4 wavefronts) takes one (row, node, key split).  All query
-// heads of the node share every key (one KV row per token), so a 32-key tile
-// staged in LDS feeds an MFMA contraction heads x keys for the logits and
-// heads x values for the output:
-//   S = Q K^T   v_mfma_f32_32x32x16_bf16, head tiles x dimension parts over waves
-//   online softmax in float32 (base-2 exponent), probabilities rounded to bf16
-//   O += P V    v_mfma_f32_32x32x16_bf16, value columns split over waves
-// A node whose keys fit one split writes its normalised output directly;
-// otherwise the split writes an unnormalised partial (O, running max, sum)
-// that the combine kernel merges in split order.
+// One workgroup (4 wavefronts) takes one (row, node, key split).  Every query
+// head of the node reads the same single KV row per key, so a 32-key tile is
+// staged once in LDS and feeds two MFMA contractions:
+//   S^T = K Q^T   (keys x heads)  v_mfma_f32_32x32x16_bf16; A = key rows from
+//                 LDS, B = this wave's query slice held in registers
+//   O^T += V^T P^T (values x heads); A = value columns read from LDS with the
+//                 gfx950 transpose read (ds_read_b64_tr_b16), B = the
+//                 probabilities straight from the S^T accumulator registers
+// With keys on the rows of S^T, each lane owns one head column: the softmax
+// row statistics are an in-lane reduction plus one cross-half shuffle, and the
+// per-head rescale of O^T is a per-lane scalar.  The logit contraction is split
+// over the key channels between the wavefronts of a head tile; they exchange
+// partial sums through LDS and add them in a fixed order, so every wavefront of
+// the tile holds bitwise identical probabilities.  Key tiles are gathered with
+// coalesced 16-byte loads one tile ahead of the math (double-buffered LDS).
+//
+// A node whose keys fit one split writes its normalised output; otherwise each
+// split writes an unnormalised partial (O, running max, sum) that the combine
+// kernel merges in split order.
 #include <algorithm>
 
 #include "node_keys.h"
@@ -18,44 +27,99 @@
 
 namespace tv {
 
-constexpr int kKT = 32;         // keys per tile
+constexpr int kKT = 32;          // keys per tile
+constexpr int kMaxChunk = 1536;  // keys per split (pointer table in LDS)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-template <int HT, int DK, int DV, int VOFF, int DROW>
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 struct AttnShape {
-  static constexpr int NP = 4 / HT;            // dimension parts of the logit contraction
-  static constexpr int KS = DK / 16;           // k-steps over the key channels
-  static constexpr int KSP = KS / NP;          // k-steps per wave
-  static constexpr int CT = DV / 4 / 32;       // 32-column output tiles per wave
-  static constexpr int QS = DK + 8;            // padded LDS row strides (elements)
-  static constexpr int KRS = DROW + 8;
-  static constexpr int PS = kKT + 8;
-  static_assert(KS % NP == 0, "key width must split over the waves");
-  static_assert(DV % 128 == 0, "value width must be a multiple of 128");
+  static constexpr int NP = NW / HT;            // wavefronts sharing a head tile
+  static constexpr int KSP = DK / 16 / NP;      // logit k-steps per wavefront
+  static constexpr int DVP = DV / NP;           // value channels per wavefront
+  static constexpr int CT = DVP / 32;           // 32-row output tiles per wavefront
+  static constexpr int CPR = DROW / 8;          // 16-byte chunks per key row
+  static constexpr int NINS = kKT * CPR / 64;   // 1 KiB LDS-copy instructions per tile
+  static constexpr int NPW = (NINS + NW - 1) / NW;  // ... per wavefront (the last ones may have one less)
+  static constexpr int TILE_BYTES = kKT * DROW * 2;
+  static_assert(NP == 4, "the k-step interleave assumes four channel parts per head tile");
+  static_assert((DK / 16) % NP == 0, "key width must split over the wavefronts");
+  static_assert(DVP % 32 == 0, "value width must split into 32-wide tiles");
+  static_assert(CPR % 8 == 0, "rows must be whole 128-byte groups");
+  // XOR swizzle of the low three bits of a row's 16-byte chunk index; with
+  // 72-chunk rows it spreads one chunk column of 16 consecutive rows over all
+  // 16 four-bank groups of the 64 LDS banks.
+  __device__ static __forceinline__ int swz(int r) { return CPR % 16 == 8 ? ((r >> 1) & 7) : (r & 7); }
+  // byte offset in a tile of element `col` of row `r`
+  __device__ static __forceinline__ int off(int r, int col) {
+    const int c = col >> 3;
+    return (r * CPR + (c & ~7) + ((c & 7) ^ swz(r))) * 16 + (col & 7) * 2;
+  }
 };
 
-template <int HT, int DK, int DV, int VOFF, int DROW>
-__global__ void __launch_bounds__(256, 1)
+// Decode the XCD-aware block index: all units of row b run on XCD b % 8
+// (workgroups are dealt to the 8 XCDs round-robin), so the rows' shared HCA,
+// window and overlapping CSA entries stay in one L2.
+__device__ __forceinline__ void unit_of(int blk, int D, int splits, int &b, int &i, int &s) {
+  const int x = blk & 7, q = blk >> 3;
+  s = q % splits;
+  const int r = q / splits;
+  i = r % D;
+  b = (r / D) * 8 + x;
+}
+
+// Barrier that waits for this wavefront's LDS traffic only: global loads in
+// flight (the next tiles) stay in flight across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+template <int N>
+__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l's 16 bytes land at LDS byte address lds + 16 l.  Issued from inline
+// assembly so that the compiler's wait-count pass does not order later LDS
+// reads of other buffers behind it; completion is awaited explicitly with
+// vm_wait<> before the barrier that publishes the tile.  M0 (the LDS base)
+// is saved and restored around the copy.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
+__global__ void __launch_bounds__(NW * 64, 1)
 attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
             const int32_t *__restrict__ depth, const uint16_t *__restrict__ scr_c4,
             const uint16_t *__restrict__ scr_c128, const uint16_t *__restrict__ q, const int32_t *__restrict__ sel,
             const int32_t *__restrict__ row_status, int chunk, int splits, float *__restrict__ part_o,
             float *__restrict__ part_ml, uint16_t *__restrict__ out, float *__restrict__ lse) {
-  using S = AttnShape<HT, DK, DV, VOFF, DROW>;
-  constexpr int R = HT * 32;  // padded head rows
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[R * S::QS];
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kKT * S::KRS];
-  __shared__ float sS[S::NP][R][kKT + 1];
-  __shared__ __attribute__((aligned(16))) uint16_t sP[R * S::PS];
-  __shared__ float sAlpha[R], sM[R], sL[R];
-  __shared__ const uint16_t *sPtr[kKT];
+  using S = AttnShape<NW, HT, DK, DV, VOFF, DROW>;
+  constexpr int NT = NW * 64;
+  constexpr int NBUF = 3;
+  __shared__ __attribute__((aligned(1024))) unsigned char sK[NBUF][S::TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) float sX[HT][S::NP][64][16];
+  __shared__ const uint16_t *sPtr[kMaxChunk];
   __shared__ int32_t path[64], hca_node[64], cnt[2];
+  __shared__ int sFlag[NW];
+  __shared__ uint2 sP[HT][S::NP][64];
+  __shared__ float sMx[HT][S::NP][32];
 
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int split = blockIdx.x % splits;
-  const int nodeg = blockIdx.x / splits;
-  const int b = nodeg / d.D, i = nodeg - b * d.D;
+  int b, i, split;
+  unit_of(blockIdx.x, d.D, splits, b, i, split);
+  if (b >= d.B) return;
   if (row_status[b] != TV_ROW_OK) return;
   const int32_t L = c.len[b];
   if (!len_ok(L, d.max_len)) return;
@@ -63,152 +127,248 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   const int k0 = split * chunk;
   if (k0 >= nk.n_keys) return;
   const int k1 = std::min(nk.n_keys, k0 + chunk);
+  const int nkeys = k1 - k0;
+  const int ntiles = (nkeys + kKT - 1) / kKT;
   const int64_t node = (int64_t)b * d.D + i;
-  const int32_t *sel_node = sel + node * d.topk;
-  const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
-
-  // queries -> LDS (rows >= H are zero)
-  const uint16_t *qn = q + node * d.H * DK;
-  for (int e = tid; e < R * (DK / 8); e += 256) {
-    const int r = e / (DK / 8), cc = (e - r * (DK / 8)) * 8;
-    uint4 v = r < d.H ? *reinterpret_cast<const uint4 *>(qn + (int64_t)r * DK + cc) : make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4 *>(sQ + r * S::QS + cc) = v;
-  }
-  if (tid < R) { sM[tid] = -INFINITY; sL[tid] = 0.f; }
-
-  f32x16 acc_o[HT][S::CT];
-#pragma unroll
-  for (int h = 0; h < HT; ++h)
-#pragma unroll
-    for (int ct = 0; ct < S::CT; ++ct) acc_o[h][ct] = f32x16{};
-
-  const float sl2 = d.scale * kLog2e;
-  const int ht_qk = wv % HT, dp = wv / HT;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
+  const int ht = wv % HT, part = wv / HT;
 
-  for (int t0 = k0; t0 < k1; t0 += kKT) {
-    if (tid < kKT) {
-      const int t = t0 + tid;
-      sPtr[tid] = t < k1 ? key_row(d, nk, b, t, sel_node, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b,
-                                   scr_c4, scr_c128, tree_u)
-                         : nullptr;
-    }
-    __syncthreads();
-    for (int e = tid; e < kKT * (DROW / 8); e += 256) {
-      const int r = e / (DROW / 8), cc = (e - r * (DROW / 8)) * 8;
-      const uint16_t *src = sPtr[r];
-      uint4 v = src ? *reinterpret_cast<const uint4 *>(src + cc) : make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4 *>(sK + r * S::KRS + cc) = v;
-    }
-    __syncthreads();
-
-    // logits: wave (head tile, dimension part)
-    {
-      f32x16 acc = f32x16{};
-      const uint16_t *qa = sQ + (ht_qk * 32 + l32) * S::QS + hi * 8;
-      const uint16_t *kb = sK + l32 * S::KRS + hi * 8;
-#pragma unroll 6
-      for (int ks = dp * S::KSP; ks < (dp + 1) * S::KSP; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(qa + ks * 16);
-        const bf16x8 bb = *reinterpret_cast<const bf16x8 *>(kb + ks * 16);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) sS[dp][ht_qk * 32 + 8 * (j >> 2) + 4 * hi + (j & 3)][l32] = acc[j];
-    }
-    __syncthreads();
-
-    // online softmax, one thread per head row
-    if (tid < R) {
-      const int h = tid;
-      const int nv = k1 - t0 < kKT ? k1 - t0 : kKT;
-      if (h < d.H) {
-        float sv[kKT];
-        float mx = sM[h];
-#pragma unroll
-        for (int t = 0; t < kKT; ++t) {
-          float s = 0.f;
-#pragma unroll
-          for (int pp = 0; pp < S::NP; ++pp) s += sS[pp][h][t];
-          s = t < nv ? s * sl2 : -INFINITY;
-          sv[t] = s;
-          mx = fmaxf(mx, s);
-        }
-        const float alpha = exp2f(sM[h] - mx);
-        float lsum = 0.f;
-#pragma unroll
-        for (int t = 0; t < kKT; ++t) {
-          const uint16_t pb = f2bf(exp2f(sv[t] - mx));
-          sP[h * S::PS + t] = pb;
-          lsum += bf2f(pb);
-        }
-        sL[h] = sL[h] * alpha + lsum;
-        sM[h] = mx;
-        sAlpha[h] = alpha;
-      } else {
-#pragma unroll
-        for (int t = 0; t < kKT; ++t) sP[h * S::PS + t] = 0;
-        sAlpha[h] = 1.f;
-      }
-    }
-    __syncthreads();
-
-    // O = O * alpha + P V ; wave owns value columns [wv*DV/4, (wv+1)*DV/4)
-#pragma unroll
-    for (int h = 0; h < HT; ++h)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float al = sAlpha[h * 32 + 8 * (j >> 2) + 4 * hi + (j & 3)];
-#pragma unroll
-        for (int ct = 0; ct < S::CT; ++ct) acc_o[h][ct][j] *= al;
-      }
-#pragma unroll
-    for (int ks = 0; ks < kKT / 16; ++ks) {
-      bf16x8 pa[HT];
-#pragma unroll
-      for (int h = 0; h < HT; ++h)
-        pa[h] = *reinterpret_cast<const bf16x8 *>(sP + (h * 32 + l32) * S::PS + ks * 16 + hi * 8);
-#pragma unroll
-      for (int ct = 0; ct < S::CT; ++ct) {
-        const int col = VOFF + wv * (DV / 4) + ct * 32 + l32;
-        const uint16_t *vb = sK + (ks * 16 + hi * 8) * S::KRS + col;
-        uint32_t w4[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) w4[u] = uint32_t(vb[(2 * u) * S::KRS]) | (uint32_t(vb[(2 * u + 1) * S::KRS]) << 16);
-        const bf16x8 vv = __builtin_bit_cast(bf16x8, make_uint4(w4[0], w4[1], w4[2], w4[3]));
-#pragma unroll
-        for (int h = 0; h < HT; ++h)
-          acc_o[h][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[h], vv, acc_o[h][ct], 0, 0, 0);
-      }
-    }
-    __syncthreads();
+  // key row pointers of this split
+  {
+    const int32_t *sel_node = sel + node * d.topk;
+    const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
+    for (int t = tid; t < nkeys; t += NT)
+      sPtr[t] = key_row(d, nk, b, k0 + t, sel_node, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4,
+                        scr_c128, tree_u);
   }
 
-  // epilogue
-  const bool single = nk.n_keys <= chunk;
+  // This wave's logit k-steps are ks = 4m + part: channels 16 ks + 8 hi of
+  // the key row (A, from LDS) and of the query (B, kept in registers).  The
+  // key chunk 8m + 2 part + hi keeps its low three bits across m, so the A
+  // address is one per-lane base plus the immediate 128 m.
+  bf16x8 qf[S::KSP];
+  {
+    const int h = ht * 32 + l32;
+    const uint16_t *qrow = q + (node * d.H + (h < d.H ? h : 0)) * DK + hi * 8;
 #pragma unroll
-  for (int h = 0; h < HT; ++h)
+    for (int m = 0; m < S::KSP; ++m) {
+      const int ks = S::NP * m + part;
+      uint4 v = h < d.H ? *reinterpret_cast<const uint4 *>(qrow + ks * 16) : make_uint4(0, 0, 0, 0);
+      qf[m] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const int aoff = S::off(l32, (2 * part + hi) * 8);
+  // Value-operand offsets for the transpose reads: rows 16 ks + 8 s + 4 hi + jj/4,
+  // columns VOFF + part*DVP + 16 (g&1) + 4 (jj&3) + 32 ct; ct's low bit changes
+  // the chunk's low bits, its upper bits add whole 128-byte groups.
+  const int g = lane >> 4, jj = lane & 15;
+  int voff[4][2];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int r = h * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
-      if (r >= d.H) continue;
-      const float inv = single ? 1.0f / sL[r] : 1.0f;
+  for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
-      for (int ct = 0; ct < S::CT; ++ct) {
-        const int col = wv * (DV / 4) + ct * 32 + l32;
-        const float v = acc_o[h][ct][j];
-        if (single)
-          out[(node * d.H + r) * DV + col] = f2bf(v * inv);
-        else
-          part_o[(((node * splits) + split) * d.H + r) * DV + col] = v;
+    for (int cp = 0; cp < 2; ++cp)
+      voff[rr][cp] = S::off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
+                            VOFF + part * S::DVP + 16 * (g & 1) + 4 * (jj & 3) + 32 * cp);
+  // Gather map: instruction k of this wave fills physical chunk P = (wv + NW k)*64 + lane,
+  // which holds logical chunk (P % CPR) ^ swz(row) of row P / CPR.
+  int gmap[S::NPW];
+#pragma unroll
+  for (int k = 0; k < S::NPW; ++k) {
+    const int P = (wv + NW * k) * 64 + lane;
+    const int r = P / S::CPR;
+    gmap[k] = r | ((((P - r * S::CPR) ^ S::swz(r)) * 16) << 8);
+  }
+  // partial-logit exchange slots: chunk u of lane l sits at u ^ ((l >> 2) & 3)
+  const int xsw = (lane >> 2) & 3;
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers before the loop
+  __syncthreads();                     // pointer table ready
+
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
+  // Rows past the split's end re-read its last key (finite data, probability forced to 0).
+  auto issue_tile = [&](int tile, int buf) {
+#pragma unroll
+    for (int k = 0; k < S::NPW; ++k) {
+      const int ins = wv + NW * k;
+      if (S::NINS % NW == 0 || ins < S::NINS) {
+        const int t = std::min(tile * kKT + (gmap[k] & 255), nkeys - 1);
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
+        dma16(src, lds_base + buf * S::TILE_BYTES + ins * 1024);
       }
     }
-  if (tid < d.H) {
-    if (single) {
-      if (lse) lse[node * d.H + tid] = (sM[tid] + __log2f(sL[tid])) * kLn2;
-    } else {
-      part_ml[(((node * splits) + split) * d.H + tid) * 2 + 0] = sM[tid];
-      part_ml[(((node * splits) + split) * d.H + tid) * 2 + 1] = sL[tid];
+  };
+
+  f32x16 acc_o[S::CT];
+  float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
+  const float sl2 = d.scale * kLog2e;
+  const bool head_live = ht * 32 + l32 < d.H;
+
+  // Softmax reference: each head's probabilities are exp2(s*scale*log2e - m_ref)
+  // with m_ref fixed for the whole split (the first tile's maximum), so the
+  // output accumulators are never rescaled inside the loop.  Probabilities may
+  // reach 2^64 (exact in the float32 sums, relative precision kept in bf16).
+  // A logit more than 64 above the reference makes the workgroup restart the
+  // split from the larger maximum; each restart raises a reference by more
+  // than 64, and at most kMaxRestarts happen.
+  //
+  // Work split of one tile: every wave of a head tile computes a partial S^T
+  // over its k-steps; wave `part` then owns key rows 8 part + 4 hi + 0..3 (its
+  // quarter of the C-layout registers): it adds the four partials of that
+  // quarter in part order, exponentiates, and publishes the bf16 probabilities.
+  // The P V contraction of every wave reads all four quarters as its B operand.
+  constexpr float kSlack = 64.0f;
+  constexpr int kMaxRestarts = 8;
+  for (int attempt = 0;; ++attempt) {
+#pragma unroll
+    for (int ct = 0; ct < S::CT; ++ct) acc_o[ct] = f32x16{};
+    l_run = 0.f;
+    const bool first = attempt == 0;
+    bool restart = false;
+    issue_tile(0, 0);
+    if (ntiles > 1) issue_tile(1, 1);
+    vm_wait<0>();
+    __syncthreads();
+
+    for (int it = 0; it < ntiles; ++it) {
+      const int buf = it % NBUF;
+      const bool ahead2 = it + 2 < ntiles;
+      const unsigned char *kt = sK[buf];
+
+      // partial S^T over this wave's k-steps
+      f32x16 sacc = f32x16{};
+#pragma unroll
+      for (int m = 0; m < S::KSP; ++m) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[m], sacc, 0, 0, 0);
+      }
+      {
+        float4 *mine = reinterpret_cast<float4 *>(&sX[ht][part][lane][0]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          mine[u ^ xsw] = make_float4(sacc[4 * u], sacc[4 * u + 1], sacc[4 * u + 2], sacc[4 * u + 3]);
+      }
+      lds_barrier();
+      // buffer (it+2)%3 was last read by P V of tile it-1, which every wave has finished
+      if (ahead2) issue_tile(it + 2, (it + 2) % NBUF);
+
+      // this wave's quarter: key rows 8 part + 4 hi + r, r = 0..3, head column l32
+      float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int p = 0; p < S::NP; ++p) {
+        const float4 t4 = reinterpret_cast<const float4 *>(&sX[ht][p][lane][0])[part ^ xsw];
+        s4.x += t4.x;
+        s4.y += t4.y;
+        s4.z += t4.z;
+        s4.w += t4.w;
+      }
+      float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+      const int nvalid = nkeys - it * kKT;
+      if (nvalid < kKT) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (8 * part + 4 * hi + r >= nvalid) sv[r] = -INFINITY;
+      }
+      float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
+      m_seen = fmaxf(m_seen, mloc);
+      if (first && it == 0) {  // the reference is the first tile's maximum over all four quarters
+        if (hi == 0) sMx[ht][part][l32] = mloc;
+        lds_barrier();
+        m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
+      }
+      const bool over = mloc > m_ref + kSlack;
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[0], sl2, -m_ref));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[1], sl2, -m_ref));
+      const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[2], sl2, -m_ref));
+      const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[3], sl2, -m_ref));
+      l_run += (p0 + p1) + (p2 + p3);
+      uint2 pq;
+      pq.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
+      pq.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p2, p3}, bf16x2));
+      sP[ht][part][lane] = pq;
+      if (lane == 0) sFlag[wv] = __any(over) ? 1 : 0;
+      if (ahead2) {
+        // tile it+1 has landed; this wave's copies of tile it+2 may still be in flight
+        if (S::NINS % NW == 0 || wv + NW * (S::NPW - 1) < S::NINS)
+          vm_wait<S::NPW>();
+        else
+          vm_wait<S::NPW - 1>();
+      } else {
+        vm_wait<0>();
+      }
+      lds_barrier();  // probabilities published, tile it+1 resident for every wave
+      int anyf = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
+      if (anyf) {
+        restart = attempt < kMaxRestarts;
+        if (restart) break;
+      }
+
+      // O^T += V^T P^T.  k-step ks covers key rows {16ks + 4hi + 0..3} (quarter
+      // 2ks) and {16ks + 8 + 4hi + 0..3} (quarter 2ks+1).
+#pragma unroll
+      for (int ks = 0; ks < kKT / 16; ++ks) {
+        const uint2 lo = sP[ht][2 * ks][lane], hq = sP[ht][2 * ks + 1][lane];
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hq.x, hq.y));
+#pragma unroll
+        for (int ct = 0; ct < S::CT; ++ct) {
+          const int imm = 128 * (ct >> 1);
+          const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4 *)(kt + voff[2 * ks][ct & 1] + imm));
+          const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4 *)(kt + voff[2 * ks + 1][ct & 1] + imm));
+          const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+                                                           v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
+          acc_o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc_o[ct], 0, 0, 0);
+        }
+      }
+    }
+    if (!restart) break;
+    // restart from the largest logit any quarter has seen, agreed through LDS
+    vm_wait<0>();
+    if (hi == 0) sMx[ht][part][l32] = m_seen;
+    __syncthreads();
+    m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
+    __syncthreads();
+  }
+  const float m_run = m_ref;
+  // row sums: this lane holds the quarter-part sum of head l32 for its half
+  l_run += __shfl_xor(l_run, 32, 64);
+  __syncthreads();
+  if (hi == 0) sMx[ht][part][l32] = l_run;
+  __syncthreads();
+  l_run = (sMx[ht][0][l32] + sMx[ht][1][l32]) + (sMx[ht][2][l32] + sMx[ht][3][l32]);
+
+  // epilogue: lane holds head ht*32 + l32, value rows part*DVP + 32ct + 8(j/4) + 4hi + (j%4)
+  const bool single = nk.n_keys <= chunk;
+  const int h = ht * 32 + l32;
+  if (head_live) {
+    const float inv = single ? 1.0f / l_run : 1.0f;
+#pragma unroll
+    for (int ct = 0; ct < S::CT; ++ct)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int col = part * S::DVP + 32 * ct + 8 * jq + 4 * hi;
+        const float v0 = acc_o[ct][4 * jq] * inv, v1 = acc_o[ct][4 * jq + 1] * inv;
+        const float v2 = acc_o[ct][4 * jq + 2] * inv, v3 = acc_o[ct][4 * jq + 3] * inv;
+        if (single) {
+          uint2 w;
+          w.x = uint32_t(f2bf(v0)) | (uint32_t(f2bf(v1)) << 16);
+          w.y = uint32_t(f2bf(v2)) | (uint32_t(f2bf(v3)) << 16);
+          *reinterpret_cast<uint2 *>(out + (node * d.H + h) * DV + col) = w;
+        } else {
+          *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * d.H + h) * DV + col) =
+              make_float4(v0, v1, v2, v3);
+        }
+      }
+    if (part == 0 && hi == 0) {
+      if (single) {
+        if (lse) lse[node * d.H + h] = (m_run + __log2f(l_run)) * kLn2;
+      } else {
+        part_ml[(((node * splits) + split) * d.H + h) * 2 + 0] = m_run;
+        part_ml[(((node * splits) + split) * d.H + h) * 2 + 1] = l_run;
+      }
     }
   }
 }
@@ -261,14 +421,15 @@ __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, CacheView c, co
   }
 }
 
-template <int HT, int DK, int DV, int VOFF, int DROW>
+template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 static hipError_t launch_attn_t(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                                 const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                                 const uint16_t *q, const int32_t *sel, const int32_t *row_status,
                                 const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
                                 hipStream_t s) {
-  const int64_t grid = (int64_t)d.B * d.D * plan.splits;
-  attn_kernel<HT, DK, DV, VOFF, DROW><<<dim3((unsigned)grid), 256, 0, s>>>(
+  if (plan.chunk > kMaxChunk) return hipErrorInvalidValue;
+  const int64_t grid = (int64_t)((d.B + 7) / 8) * 8 * d.D * plan.splits;
+  attn_kernel<NW, HT, DK, DV, VOFF, DROW><<<dim3((unsigned)grid), NW * 64, 0, s>>>(
       d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status, plan.chunk, plan.splits, part_o, part_ml,
       out, lse);
   return hipGetLastError();
@@ -279,11 +440,11 @@ hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tre
                        const int32_t *sel, const int32_t *row_status, const SplitPlan &plan, float *part_o,
                        float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
   if (d.H == 64 && d.d_k == 576 && d.d_v == 512 && d.v_off == 0 && d.d_row == 576)
-    return launch_attn_t<2, 576, 512, 0, 576>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status, plan,
-                                              part_o, part_ml, out, lse, s);
+    return launch_attn_t<8, 2, 576, 512, 0, 576>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
+                                                 plan, part_o, part_ml, out, lse, s);
   if (d.H == 8 && d.d_k == 128 && d.d_v == 128 && d.v_off == 128 && d.d_row == 256)
-    return launch_attn_t<1, 128, 128, 128, 256>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
-                                                plan, part_o, part_ml, out, lse, s);
+    return launch_attn_t<4, 1, 128, 128, 128, 256>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
+                                                   plan, part_o, part_ml, out, lse, s);
   return hipErrorInvalidValue;
 }
 

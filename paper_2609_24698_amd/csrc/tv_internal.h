@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/tv.h"
+#include "tv.h"
 
 namespace tv {
 
