@@ -1,24 +1,27 @@
 // Branch-aware verify attention over CSA / HCA / window keys.
 //
-// One workgroup (4 wavefronts) takes one (row, node, key split).  Every query
-// head of the node reads the same single KV row per key, so a 32-key tile is
-// staged once in LDS and feeds two MFMA contractions:
-//   S^T = K Q^T   (keys x heads)  v_mfma_f32_32x32x16_bf16; A = key rows from
-//                 LDS, B = this wave's query slice held in registers
-//   O^T += V^T P^T (values x heads); A = value columns read from LDS with the
-//                 gfx950 transpose read (ds_read_b64_tr_b16), B = the
-//                 probabilities straight from the S^T accumulator registers
-// With keys on the rows of S^T, each lane owns one head column: the softmax
-// row statistics are an in-lane reduction plus one cross-half shuffle, and the
-// per-head rescale of O^T is a per-lane scalar.  The logit contraction is split
-// over the key channels between the wavefronts of a head tile; they exchange
-// partial sums through LDS and add them in a fixed order, so every wavefront of
-// the tile holds bitwise identical probabilities.  Key tiles are gathered with
-// coalesced 16-byte loads one tile ahead of the math (double-buffered LDS).
+// One workgroup (8 wavefronts, two per SIMD) takes one (row, node, key
+// split).  Every query head of the node reads the same single KV row per key,
+// so a 32-key tile is gathered once into LDS (direct global->LDS copies, two
+// tiles ahead of the math) and feeds two MFMA contractions
+// (v_mfma_f32_32x32x16_bf16, float32 accumulation):
+//   S^T = K Q^T     keys x heads.  Wave (head tile ht, part p) holds the
+//                   queries of 32 heads for a quarter of the key channels and
+//                   computes a partial S^T; wave p then owns key rows
+//                   8p + 4hi + 0..3 of the tile: it adds the four partials in
+//                   part order, exponentiates and publishes bf16 P to LDS.
+//   O^T += V^T P^T  value channels x heads.  Wave w owns value channels
+//                   w*DV/8.. for all heads, so each value element crosses the
+//                   slow LDS transpose path (ds_read_b64_tr_b16) exactly once
+//                   per tile; P comes back from LDS with plain 8-byte reads.
+// Keys on the rows of S^T give each lane one head column, so the softmax
+// statistics are per lane.  The loop is software-pipelined: the P V of tile t
+// and the logits of tile t+1 form one MFMA phase, the probabilities of tile
+// t+1 the next, with one barrier between phases.
 //
 // A node whose keys fit one split writes its normalised output; otherwise each
-// split writes an unnormalised partial (O, running max, sum) that the combine
-// kernel merges in split order.
+// split writes an unnormalised partial (O, reference max, sum) that the
+// combine kernel merges in split order.
 #include <algorithm>
 
 #include "node_keys.h"
@@ -39,15 +42,15 @@ template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 struct AttnShape {
   static constexpr int NP = NW / HT;            // wavefronts sharing a head tile
   static constexpr int KSP = DK / 16 / NP;      // logit k-steps per wavefront
-  static constexpr int DVP = DV / NP;           // value channels per wavefront
-  static constexpr int CT = DVP / 32;           // 32-row output tiles per wavefront
+  static constexpr int DVW = DV / NW;           // value channels per wavefront (all heads)
+  static constexpr int CT = DVW / 32;           // 32-row output tiles per wavefront and head tile
   static constexpr int CPR = DROW / 8;          // 16-byte chunks per key row
   static constexpr int NINS = kKT * CPR / 64;   // 1 KiB LDS-copy instructions per tile
   static constexpr int NPW = (NINS + NW - 1) / NW;  // ... per wavefront (the last ones may have one less)
   static constexpr int TILE_BYTES = kKT * DROW * 2;
   static_assert(NP == 4, "the k-step interleave assumes four channel parts per head tile");
   static_assert((DK / 16) % NP == 0, "key width must split over the wavefronts");
-  static_assert(DVP % 32 == 0, "value width must split into 32-wide tiles");
+  static_assert(DVW % 32 == 0, "value width must split into 32-wide tiles");
   static_assert(CPR % 8 == 0, "rows must be whole 128-byte groups");
   // XOR swizzle of the low three bits of a row's 16-byte chunk index; with
   // 72-chunk rows it spreads one chunk column of 16 consecutive rows over all
@@ -81,8 +84,9 @@ __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" :
 // lane l's 16 bytes land at LDS byte address lds + 16 l.  Issued from inline
 // assembly so that the compiler's wait-count pass does not order later LDS
 // reads of other buffers behind it; completion is awaited explicitly with
-// vm_wait<> before the barrier that publishes the tile.  M0 (the LDS base)
-// is saved and restored around the copy.
+// vm_wait<> before the barrier that publishes the tile (both carry memory
+// clobbers, the copy itself needs none: nothing reads its destination before
+// that barrier).  M0 (the LDS base) is saved and restored around the copy.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
   uint32_t saved;
   asm volatile(
@@ -92,8 +96,7 @@ __device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
       "global_load_lds_dwordx4 %1, off\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds))
-      : "memory");
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds)));
 }
 
 typedef __attribute__((ext_vector_type(2))) float f32x2;
@@ -116,6 +119,7 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   __shared__ int sFlag[NW];
   __shared__ uint2 sP[HT][S::NP][64];
   __shared__ float sMx[HT][S::NP][32];
+  __shared__ float sRef[HT][32];
 
   int b, i, split;
   unit_of(blockIdx.x, d.D, splits, b, i, split);
@@ -160,16 +164,15 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   }
   const int aoff = S::off(l32, (2 * part + hi) * 8);
   // Value-operand offsets for the transpose reads: rows 16 ks + 8 s + 4 hi + jj/4,
-  // columns VOFF + part*DVP + 16 (g&1) + 4 (jj&3) + 32 ct; ct's low bit changes
-  // the chunk's low bits, its upper bits add whole 128-byte groups.
+  // columns VOFF + wv*DVW + 16 (g&1) + 4 (jj&3) + 32 ct.
   const int g = lane >> 4, jj = lane & 15;
-  int voff[4][2];
+  int voff[4][S::CT];
 #pragma unroll
   for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
-    for (int cp = 0; cp < 2; ++cp)
-      voff[rr][cp] = S::off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
-                            VOFF + part * S::DVP + 16 * (g & 1) + 4 * (jj & 3) + 32 * cp);
+    for (int ct = 0; ct < S::CT; ++ct)
+      voff[rr][ct] = S::off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
+                            VOFF + wv * S::DVW + 16 * (g & 1) + 4 * (jj & 3) + 32 * ct);
   // Gather map: instruction k of this wave fills physical chunk P = (wv + NW k)*64 + lane,
   // which holds logical chunk (P % CPR) ^ swz(row) of row P / CPR.
   int gmap[S::NPW];
@@ -187,21 +190,24 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
   // Rows past the split's end re-read its last key (finite data, probability forced to 0).
   auto issue_tile = [&](int tile, int buf) {
+    const unsigned char *src[S::NPW];
+#pragma unroll
+    for (int k = 0; k < S::NPW; ++k) {  // all pointer reads first: one LDS wait
+      const int t = std::min(tile * kKT + (gmap[k] & 255), nkeys - 1);
+      src[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
+    }
 #pragma unroll
     for (int k = 0; k < S::NPW; ++k) {
       const int ins = wv + NW * k;
-      if (S::NINS % NW == 0 || ins < S::NINS) {
-        const int t = std::min(tile * kKT + (gmap[k] & 255), nkeys - 1);
-        const unsigned char *src = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
-        dma16(src, lds_base + buf * S::TILE_BYTES + ins * 1024);
-      }
+      if (S::NINS % NW == 0 || ins < S::NINS) dma16(src[k], lds_base + buf * S::TILE_BYTES + ins * 1024);
     }
   };
+  // vmcnt bound that leaves this wave's copies of the newest tile in flight
+  const bool full_share = S::NINS % NW == 0 || wv + NW * (S::NPW - 1) < S::NINS;
 
-  f32x16 acc_o[S::CT];
+  f32x16 acc_o[HT][S::CT];
   float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
   const float sl2 = d.scale * kLog2e;
-  const bool head_live = ht * 32 + l32 < d.H;
 
   // Softmax reference: each head's probabilities are exp2(s*scale*log2e - m_ref)
   // with m_ref fixed for the whole split (the first tile's maximum), so the
@@ -218,9 +224,108 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   // The P V contraction of every wave reads all four quarters as its B operand.
   constexpr float kSlack = 64.0f;
   constexpr int kMaxRestarts = 8;
+
+  // Logits of tile `it` (buffer it % 3): this wave's partial S^T, published for the reduce-scatter.
+  auto qk_tile = [&](int it) {
+    const unsigned char *kt = sK[it % NBUF];
+    f32x16 sacc = f32x16{};
+#pragma unroll
+    for (int m = 0; m < S::KSP; ++m) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[m], sacc, 0, 0, 0);
+    }
+    float4 *mine = reinterpret_cast<float4 *>(&sX[ht][part][lane][0]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      mine[u ^ xsw] = make_float4(sacc[4 * u], sacc[4 * u + 1], sacc[4 * u + 2], sacc[4 * u + 3]);
+  };
+  // Probabilities of tile `it` for this wave's quarter (key rows 8 part + 4 hi + 0..3):
+  // sum the four partials in part order, exponentiate against the reference,
+  // publish bf16 P and the overflow flag.
+  auto softmax_tile = [&](int it, bool set_ref) {
+    float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int p = 0; p < S::NP; ++p) {
+      const float4 t4 = reinterpret_cast<const float4 *>(&sX[ht][p][lane][0])[part ^ xsw];
+      s4.x += t4.x;
+      s4.y += t4.y;
+      s4.z += t4.z;
+      s4.w += t4.w;
+    }
+    float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+    const int nvalid = nkeys - it * kKT;
+    if (nvalid < kKT) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (8 * part + 4 * hi + r >= nvalid) sv[r] = -INFINITY;
+    }
+    float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
+    m_seen = fmaxf(m_seen, mloc);
+    if (set_ref) {  // the reference is the first tile's maximum over all four quarters
+      if (hi == 0) sMx[ht][part][l32] = mloc;
+      lds_barrier();
+      m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
+    }
+    const bool over = mloc > m_ref + kSlack;
+    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[0], sl2, -m_ref));
+    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[1], sl2, -m_ref));
+    const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[2], sl2, -m_ref));
+    const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[3], sl2, -m_ref));
+    l_run += (p0 + p1) + (p2 + p3);
+    uint2 pq;
+    pq.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
+    pq.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p2, p3}, bf16x2));
+    sP[ht][part][lane] = pq;
+    if (lane == 0) sFlag[wv] = __any(over) ? 1 : 0;
+  };
+  // O^T += V^T P^T for tile `it`, this wave's value channels, every head tile.
+  // k-step ks covers key rows {16ks + 4hi + 0..3} (quarter 2ks) and
+  // {16ks + 8 + 4hi + 0..3} (quarter 2ks+1).
+  auto pv_tile = [&](int it) {
+    const unsigned char *kt = sK[it % NBUF];
+#pragma unroll
+    for (int ks = 0; ks < kKT / 16; ++ks) {
+      bf16x8 pb[HT];
+#pragma unroll
+      for (int t = 0; t < HT; ++t) {
+        const uint2 lo = sP[t][2 * ks][lane], hq = sP[t][2 * ks + 1][lane];
+        pb[t] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hq.x, hq.y));
+      }
+#pragma unroll
+      for (int ct = 0; ct < S::CT; ++ct) {
+        const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
+        const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks + 1][ct]));
+        const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+                                                         v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
+#pragma unroll
+        for (int t = 0; t < HT; ++t)
+          acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[t], acc_o[t][ct], 0, 0, 0);
+      }
+    }
+  };
+  // Tile t+2 copy issue and the wait for tile t+1 (Y phase of tile t).
+  auto advance = [&](int t) {
+    if (t + 2 < ntiles) {
+      issue_tile(t + 2, (t + 2) % NBUF);  // buffer of tile t-1, read by every wave before this phase
+      if (full_share)
+        vm_wait<S::NPW>();
+      else
+        vm_wait<S::NPW - 1>();
+    } else {
+      vm_wait<0>();
+    }
+  };
+
+  // Software pipeline over tiles, two barriers per tile:
+  //   X(t): P V of tile t and the logits of tile t+1 (independent MFMA chains)
+  //   Y(t+1): probabilities of tile t+1, copy of tile t+3, wait for tile t+2
+  // Tiles t and t+1 are resident during X(t); tile t+2 is in flight.
   for (int attempt = 0;; ++attempt) {
 #pragma unroll
-    for (int ct = 0; ct < S::CT; ++ct) acc_o[ct] = f32x16{};
+    for (int t = 0; t < HT; ++t)
+#pragma unroll
+      for (int ct = 0; ct < S::CT; ++ct) acc_o[t][ct] = f32x16{};
     l_run = 0.f;
     const bool first = attempt == 0;
     bool restart = false;
@@ -228,146 +333,85 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
     if (ntiles > 1) issue_tile(1, 1);
     vm_wait<0>();
     __syncthreads();
+    qk_tile(0);
+    lds_barrier();
+    softmax_tile(0, first);
+    advance(0);
+    lds_barrier();
 
     for (int it = 0; it < ntiles; ++it) {
-      const int buf = it % NBUF;
-      const bool ahead2 = it + 2 < ntiles;
-      const unsigned char *kt = sK[buf];
-
-      // partial S^T over this wave's k-steps
-      f32x16 sacc = f32x16{};
-#pragma unroll
-      for (int m = 0; m < S::KSP; ++m) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
-        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[m], sacc, 0, 0, 0);
-      }
-      {
-        float4 *mine = reinterpret_cast<float4 *>(&sX[ht][part][lane][0]);
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          mine[u ^ xsw] = make_float4(sacc[4 * u], sacc[4 * u + 1], sacc[4 * u + 2], sacc[4 * u + 3]);
-      }
-      lds_barrier();
-      // buffer (it+2)%3 was last read by P V of tile it-1, which every wave has finished
-      if (ahead2) issue_tile(it + 2, (it + 2) % NBUF);
-
-      // this wave's quarter: key rows 8 part + 4 hi + r, r = 0..3, head column l32
-      float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-      for (int p = 0; p < S::NP; ++p) {
-        const float4 t4 = reinterpret_cast<const float4 *>(&sX[ht][p][lane][0])[part ^ xsw];
-        s4.x += t4.x;
-        s4.y += t4.y;
-        s4.z += t4.z;
-        s4.w += t4.w;
-      }
-      float sv[4] = {s4.x, s4.y, s4.z, s4.w};
-      const int nvalid = nkeys - it * kKT;
-      if (nvalid < kKT) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (8 * part + 4 * hi + r >= nvalid) sv[r] = -INFINITY;
-      }
-      float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
-      m_seen = fmaxf(m_seen, mloc);
-      if (first && it == 0) {  // the reference is the first tile's maximum over all four quarters
-        if (hi == 0) sMx[ht][part][l32] = mloc;
-        lds_barrier();
-        m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
-      }
-      const bool over = mloc > m_ref + kSlack;
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[0], sl2, -m_ref));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[1], sl2, -m_ref));
-      const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[2], sl2, -m_ref));
-      const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[3], sl2, -m_ref));
-      l_run += (p0 + p1) + (p2 + p3);
-      uint2 pq;
-      pq.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
-      pq.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p2, p3}, bf16x2));
-      sP[ht][part][lane] = pq;
-      if (lane == 0) sFlag[wv] = __any(over) ? 1 : 0;
-      if (ahead2) {
-        // tile it+1 has landed; this wave's copies of tile it+2 may still be in flight
-        if (S::NINS % NW == 0 || wv + NW * (S::NPW - 1) < S::NINS)
-          vm_wait<S::NPW>();
-        else
-          vm_wait<S::NPW - 1>();
-      } else {
-        vm_wait<0>();
-      }
-      lds_barrier();  // probabilities published, tile it+1 resident for every wave
+      const bool more = it + 1 < ntiles;
+      pv_tile(it);
+      if (more) qk_tile(it + 1);
       int anyf = 0;
 #pragma unroll
       for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
-      if (anyf) {
+      if (anyf) {  // probabilities of tile it overflowed the reference
         restart = attempt < kMaxRestarts;
         if (restart) break;
       }
-
-      // O^T += V^T P^T.  k-step ks covers key rows {16ks + 4hi + 0..3} (quarter
-      // 2ks) and {16ks + 8 + 4hi + 0..3} (quarter 2ks+1).
-#pragma unroll
-      for (int ks = 0; ks < kKT / 16; ++ks) {
-        const uint2 lo = sP[ht][2 * ks][lane], hq = sP[ht][2 * ks + 1][lane];
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hq.x, hq.y));
-#pragma unroll
-        for (int ct = 0; ct < S::CT; ++ct) {
-          const int imm = 128 * (ct >> 1);
-          const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4 *)(kt + voff[2 * ks][ct & 1] + imm));
-          const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4 *)(kt + voff[2 * ks + 1][ct & 1] + imm));
-          const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
-                                                           v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
-          acc_o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc_o[ct], 0, 0, 0);
-        }
-      }
+      if (!more) break;
+      lds_barrier();
+      softmax_tile(it + 1, false);
+      advance(it + 1);
+      lds_barrier();
     }
     if (!restart) break;
     // restart from the largest logit any quarter has seen, agreed through LDS
     vm_wait<0>();
+    __syncthreads();
     if (hi == 0) sMx[ht][part][l32] = m_seen;
     __syncthreads();
     m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
     __syncthreads();
   }
-  const float m_run = m_ref;
-  // row sums: this lane holds the quarter-part sum of head l32 for its half
+  // Row sums and references per head tile: wave (ht, part) holds the sum over
+  // its key quarter for head ht*32 + l32 (halves combined across hi).
   l_run += __shfl_xor(l_run, 32, 64);
   __syncthreads();
-  if (hi == 0) sMx[ht][part][l32] = l_run;
+  if (hi == 0) {
+    sMx[ht][part][l32] = l_run;
+    sRef[ht][l32] = m_ref;  // identical across the parts of a head tile
+  }
   __syncthreads();
-  l_run = (sMx[ht][0][l32] + sMx[ht][1][l32]) + (sMx[ht][2][l32] + sMx[ht][3][l32]);
+  float lsum[HT], mref[HT];
+#pragma unroll
+  for (int t = 0; t < HT; ++t) {
+    lsum[t] = (sMx[t][0][l32] + sMx[t][1][l32]) + (sMx[t][2][l32] + sMx[t][3][l32]);
+    mref[t] = sRef[t][l32];
+  }
 
-  // epilogue: lane holds head ht*32 + l32, value rows part*DVP + 32ct + 8(j/4) + 4hi + (j%4)
+  // epilogue: lane holds, per head tile t, head t*32 + l32 and value rows
+  // wv*DVW + 32ct + 8(j/4) + 4hi + (j%4)
   const bool single = nk.n_keys <= chunk;
-  const int h = ht * 32 + l32;
-  if (head_live) {
-    const float inv = single ? 1.0f / l_run : 1.0f;
+#pragma unroll
+  for (int t = 0; t < HT; ++t) {
+    const int h = t * 32 + l32;
+    if (h >= d.H) continue;
+    const float inv = single ? 1.0f / lsum[t] : 1.0f;
 #pragma unroll
     for (int ct = 0; ct < S::CT; ++ct)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const int col = part * S::DVP + 32 * ct + 8 * jq + 4 * hi;
-        const float v0 = acc_o[ct][4 * jq] * inv, v1 = acc_o[ct][4 * jq + 1] * inv;
-        const float v2 = acc_o[ct][4 * jq + 2] * inv, v3 = acc_o[ct][4 * jq + 3] * inv;
+        const int col = wv * S::DVW + 32 * ct + 8 * jq + 4 * hi;
+        const float v0 = acc_o[t][ct][4 * jq] * inv, v1 = acc_o[t][ct][4 * jq + 1] * inv;
+        const float v2 = acc_o[t][ct][4 * jq + 2] * inv, v3 = acc_o[t][ct][4 * jq + 3] * inv;
         if (single) {
           uint2 w;
-          w.x = uint32_t(f2bf(v0)) | (uint32_t(f2bf(v1)) << 16);
-          w.y = uint32_t(f2bf(v2)) | (uint32_t(f2bf(v3)) << 16);
+          w.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v0, v1}, bf16x2));
+          w.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v2, v3}, bf16x2));
           *reinterpret_cast<uint2 *>(out + (node * d.H + h) * DV + col) = w;
         } else {
           *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * d.H + h) * DV + col) =
               make_float4(v0, v1, v2, v3);
         }
       }
-    if (part == 0 && hi == 0) {
+    if (wv == 0 && hi == 0) {
       if (single) {
-        if (lse) lse[node * d.H + h] = (m_run + __log2f(l_run)) * kLn2;
+        if (lse) lse[node * d.H + h] = (mref[t] + __log2f(lsum[t])) * kLn2;
       } else {
-        part_ml[(((node * splits) + split) * d.H + h) * 2 + 0] = m_run;
-        part_ml[(((node * splits) + split) * d.H + h) * 2 + 1] = l_run;
+        part_ml[(((node * splits) + split) * d.H + h) * 2 + 0] = mref[t];
+        part_ml[(((node * splits) + split) * d.H + h) * 2 + 1] = lsum[t];
       }
     }
   }
