@@ -18,7 +18,7 @@ static bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 static bool shape_supported(const tv_dims &d) {
   const bool mla = d.H == 64 && d.d_row == 576 && d.d_k == 576 && d.v_off == 0 && d.d_v == 512;
   const bool mha = d.H == 8 && d.d_row == 256 && d.d_k == 128 && d.v_off == 128 && d.d_v == 128;
-  return (mla || mha) && d.d_idx == 64 && pow2(d.H_idx) && d.H_idx <= 64;
+  return (mla || mha) && d.d_idx == 64 && pow2(d.H_idx) && d.H_idx <= 64 && d.d_row + d.d_idx <= 1024;
 }
 
 // Dimension checks shared by every entry point.

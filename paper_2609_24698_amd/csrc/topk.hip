@@ -6,9 +6,12 @@
 // scratch indexer keys): a node never sees an entry compressed on another
 // branch (Sec. 3.1, Sec. 4.1).
 //
-// Selection is an exact radix select on order-preserving 32-bit keys
-// (11 + 11 + 10 bit digits, histograms in LDS), then an ordered compaction:
-// every key above the threshold plus the lowest-index keys equal to it.
+// Selection is an exact radix select on order-preserving 32-bit keys (four
+// 8-bit digits, one LDS histogram per wavefront), followed by an ordered
+// compaction in index order: wavefront ballots rank the keys above the
+// threshold and the lowest-index keys equal to it.  Keys live in LDS when the
+// candidate list fits, otherwise they are re-derived from the global scores
+// on every pass.
 #include <algorithm>
 
 #include "tv_common.h"
@@ -17,26 +20,7 @@
 namespace tv {
 
 constexpr int kMaxScratch = 64;
-
-__device__ int block_excl_scan_i(int v, int *tmp, int *total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) tmp[wv] = x;
-  __syncthreads();
-  int base = 0, tot = 0;
-  for (int k = 0; k < 4; ++k) {
-    if (k < wv) base += tmp[k];
-    tot += tmp[k];
-  }
-  __syncthreads();
-  *total = tot;
-  return base + x - v;
-}
+constexpr int kLdsKeys = 16384 + 256;  // candidates held in LDS (65 KiB): rows up to L = 65536 plus a path
 
 __global__ void __launch_bounds__(256) topk_kernel(tv_dims d, CacheView c, const uint64_t *__restrict__ anc,
                                                    const int32_t *__restrict__ depth,
@@ -45,11 +29,13 @@ __global__ void __launch_bounds__(256) topk_kernel(tv_dims d, CacheView c, const
                                                    const uint16_t *__restrict__ w_idx,
                                                    const float *__restrict__ scores, int score_stride,
                                                    int32_t *__restrict__ sel, int32_t *__restrict__ row_status) {
-  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t keys[kLdsKeys];
+  __shared__ uint32_t hist[4][256];
   __shared__ float scr_score[kMaxScratch];
   __shared__ int32_t scr_node[kMaxScratch];
-  __shared__ int scan_tmp[4];
-  __shared__ uint32_t found[2];  // digit, count of keys above the digit's bin
+  __shared__ int wcnt[2][16];
+  __shared__ float hterm[16][64];
+  __shared__ uint32_t found[2];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int b = blockIdx.x / d.D;
   const int i = blockIdx.x - b * d.D;
@@ -74,19 +60,33 @@ __global__ void __launch_bounds__(256) topk_kernel(tv_dims d, CacheView c, const
   __syncthreads();
   int nscr = 0;
   while (nscr < d.D && scr_node[nscr] >= 0) ++nscr;
-  if (wv == 0) {
-    for (int t = 0; t < nscr; ++t) {
-      const uint16_t *key = scr_c4 + ((int64_t)b * d.D + scr_node[t]) * d_u + d.d_row;
-      float s = 0.f;
-      for (int h = 0; h < d.H_idx; ++h) {
-        const uint16_t *qh = q_idx + (node * d.H_idx + h) * 64;
-        const float dot = wave_sum(bf2f(qh[lane]) * bf2f(key[lane]));
-        s += bf2f(w_idx[node * d.H_idx + h]) * fmaxf(dot, 0.f);
+  // scores of the path entries: wave w takes heads w, w+4, ..; lane = key channel;
+  // every operand is loaded before the first reduction
+  for (int t0 = 0; t0 < nscr; t0 += 16) {
+    const int nt = std::min(16, nscr - t0);
+    float kv[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      kv[t] = t < nt ? bf2f(scr_c4[((int64_t)b * d.D + scr_node[t0 + t]) * d_u + d.d_row + lane]) : 0.f;
+    for (int h = wv; h < d.H_idx; h += 4) {
+      const float qv = bf2f(q_idx[(node * d.H_idx + h) * 64 + lane]);
+      const float wh = bf2f(w_idx[node * d.H_idx + h]);
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        if (t < nt) {
+          const float dot = wave_sum(qv * kv[t]);
+          if (lane == 0) hterm[t][h] = wh * fmaxf(dot, 0.f);
+        }
       }
-      if (lane == 0) scr_score[t] = s;
     }
+    __syncthreads();
+    if (tid < nt) {
+      float sum = 0.f;
+      for (int h = 0; h < d.H_idx; ++h) sum += hterm[tid][h];  // head order
+      scr_score[t0 + tid] = sum;
+    }
+    __syncthreads();
   }
-  __syncthreads();
 
   const int n = n4 + nscr;
   int32_t *out = sel + node * d.topk;
@@ -95,72 +95,134 @@ __global__ void __launch_bounds__(256) topk_kernel(tv_dims d, CacheView c, const
     for (int t = tid; t < d.topk; t += 256) out[t] = t < n ? t : -1;
     return;
   }
-  auto key_of = [&](int s) -> uint32_t { return score_key(s < n4 ? sc[s] : scr_score[s - n4]); };
+  const bool in_lds = n <= kLdsKeys;
+  if (in_lds) {  // sixteen loads in flight per thread
+    for (int s0 = 0; s0 < n; s0 += 256 * 16) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int s = s0 + tid + 256 * u;
+        v[u] = s < n4 ? sc[s] : (s < n ? scr_score[s - n4] : 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int s = s0 + tid + 256 * u;
+        if (s < n) keys[s] = score_key(v[u]);
+      }
+    }
+  }
+  __syncthreads();
+  auto key_of = [&](int s) -> uint32_t {
+    return in_lds ? keys[s] : score_key(s < n4 ? sc[s] : scr_score[s - n4]);
+  };
 
-  // radix select of the k-th largest key
+  // radix select of the k-th largest key, 8 bits per pass
   uint32_t prefix = 0, pmask = 0;
   int remaining = d.topk;
-  const int shifts[3] = {21, 10, 0};
-  const int widths[3] = {11, 11, 10};
-  for (int pass = 0; pass < 3; ++pass) {
-    const int sh = shifts[pass], nb = 1 << widths[pass];
-    for (int t = tid; t < 2048; t += 256) hist[t] = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int sh = 24 - 8 * pass;
+    for (int t = tid; t < 1024; t += 256) (&hist[0][0])[t] = 0;
     __syncthreads();
-    for (int s = tid; s < n; s += 256) {
-      const uint32_t k = key_of(s);
-      if ((k & pmask) == prefix) atomicAdd(&hist[(k >> sh) & (nb - 1)], 1u);
+    for (int s0 = 0; s0 < n; s0 += 256 * 16) {  // sixteen key reads in flight
+      uint32_t kk[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int s = s0 + tid + 256 * u;
+        kk[u] = s < n ? key_of(s) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int s = s0 + tid + 256 * u;
+        if (s < n && (kk[u] & pmask) == prefix) atomicAdd(&hist[wv][(kk[u] >> sh) & 255], 1u);
+      }
     }
     __syncthreads();
-    // thread t owns bins [nb - 8(t+1), nb - 8t), scanned from the top bin down
-    const int per = nb / 256;
-    const int hi = nb - per * tid;
-    int local = 0;
-    for (int q = 1; q <= per; ++q) local += hist[hi - q];
-    int total;
-    int above = block_excl_scan_i(local, scan_tmp, &total);
-    for (int q = 1; q <= per; ++q) {
-      const int bin = hi - q;
-      const int h = hist[bin];
-      if (above < remaining && remaining <= above + h) {
-        found[0] = bin;
-        found[1] = above;
+    if (wv == 0) {  // lane owns bins 255-4l .. 252-4l, scanned from the top bin down
+      int cntv[4], local = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int bin = 255 - 4 * lane - u;
+        cntv[u] = (int)(hist[0][bin] + hist[1][bin] + hist[2][bin] + hist[3][bin]);
+        local += cntv[u];
       }
-      above += h;
+      int incl = local;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      int above = incl - local;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (above < remaining && remaining <= above + cntv[u]) {
+          found[0] = 255 - 4 * lane - u;
+          found[1] = above;
+        }
+        above += cntv[u];
+      }
     }
     __syncthreads();
     const uint32_t digit = found[0];
     remaining -= (int)found[1];
     prefix |= digit << sh;
-    pmask |= uint32_t(nb - 1) << sh;
+    pmask |= 255u << sh;
     __syncthreads();
   }
   const uint32_t T = prefix;  // the k-th largest key; take `remaining` keys equal to it
 
-  // ordered compaction over contiguous per-thread segments
-  const int seg = (n + 255) / 256;
-  const int s0 = std::min(n, tid * seg), s1 = std::min(n, s0 + seg);
-  int eq = 0;
-  for (int s = s0; s < s1; ++s) eq += key_of(s) == T;
-  int tot;
-  int eq_before = block_excl_scan_i(eq, scan_tmp, &tot);
-  int take = 0;
-  {
-    int e = eq_before;
-    for (int s = s0; s < s1; ++s) {
-      const uint32_t k = key_of(s);
-      if (k > T) ++take;
-      else if (k == T && e++ < remaining) ++take;
+  // Ordered compaction in chunks of 1024 consecutive indices (element
+  // base + 256 u + tid for u = 0..3): wave ballots give in-wave ranks, the
+  // per-(u, wave) counts in LDS give every element's offset.
+  int out_before = 0, eq_before = 0;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int base = 0; base < n; base += 1024) {
+    bool gt[4], eq[4];
+    uint64_t beq[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int s = base + 256 * u + tid;
+      const uint32_t k = s < n ? key_of(s) : 0u;
+      gt[u] = s < n && k > T;
+      eq[u] = s < n && k == T;
+      beq[u] = __ballot(eq[u]);
+      if (lane == 0) wcnt[0][4 * u + wv] = __popcll(beq[u]);
     }
-  }
-  int pos = block_excl_scan_i(take, scan_tmp, &tot);
-  {
-    int e = eq_before;
-    for (int s = s0; s < s1; ++s) {
-      const uint32_t k = key_of(s);
-      bool f = k > T;
-      if (!f && k == T) f = e++ < remaining;
-      if (f) out[pos++] = s;
+    __syncthreads();
+    // exclusive scan of the 16 (u, wave) counts, redundantly in every wave
+    auto scan16 = [&](const int *cnt, int &excl, int &tot) {
+      const int v = lane < 16 ? cnt[lane] : 0;
+      int inc = v;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const int y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+      }
+      excl = inc - v;
+      tot = __shfl(inc, 15, 64);
+    };
+    int eq_excl, eq_tot;
+    scan16(wcnt[0], eq_excl, eq_tot);
+    bool take[4];
+    uint64_t bt[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int off = eq_before + __shfl(eq_excl, 4 * u + wv, 64);
+      take[u] = gt[u] || (eq[u] && off + __popcll(beq[u] & lt_mask) < remaining);
+      bt[u] = __ballot(take[u]);
+      if (lane == 0) wcnt[1][4 * u + wv] = __popcll(bt[u]);
     }
+    __syncthreads();
+    int o_excl, o_tot;
+    scan16(wcnt[1], o_excl, o_tot);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int off = out_before + __shfl(o_excl, 4 * u + wv, 64);
+      if (take[u]) out[off + __popcll(bt[u] & lt_mask)] = base + 256 * u + tid;
+    }
+    out_before += o_tot;
+    eq_before += eq_tot;
+    __syncthreads();
+    if (out_before >= d.topk) break;
   }
 }
 
