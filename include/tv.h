@@ -33,6 +33,9 @@
  *   - Every pointer is device memory owned by the caller.  The library never
  *     allocates device memory and keeps no state between calls besides device
  *     properties and the optional profiling records.
+ *   - Every buffer must start on a 16-byte boundary (the kernels move rows
+ *     with 16-byte accesses); a misaligned pointer is TV_ERR_INVALID_ARG.
+ *   - The verify workspace must be 256-byte aligned.
  *   - Calls enqueue work on `stream` and return without synchronising the
  *     host.  Issue them in the order mask -> compress -> verify -> commit.
  *   - Floating-point buffers hold bfloat16 bit patterns (uint16_t) unless

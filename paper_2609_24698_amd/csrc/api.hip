@@ -43,6 +43,16 @@ static bool cache_complete(const tv_cache *c) {
          c->c128_cap && c->len;
 }
 
+// Kernels move rows with 16-byte loads and stores; every buffer must allow them.
+static bool a16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+template <typename... P>
+static bool all_a16(const P *...p) {
+  return (a16(p) && ...);
+}
+static bool cache_a16(const tv_cache *c) {
+  return all_a16(c->ring, c->c4, c->c4_idx, c->c128, c->c4_base, c->c4_cap, c->c128_base, c->c128_cap, c->len);
+}
+
 // The library only runs on gfx950; the answer is cached per device.
 static tv_status check_device() {
   static std::mutex mu;
@@ -159,6 +169,7 @@ tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
   if (!parents || !anc || !depth || !row_status) return TV_ERR_INVALID_ARG;
+  if (!all_a16(parents, anc, depth, row_status)) return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("tree_mask", launch_mask(*dims, parents, anc, depth, row_status, stream));
   return TV_OK;
@@ -170,6 +181,8 @@ tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const u
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
   if (!cache_complete(cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status))
     return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("branch_compress", launch_compress(*dims, view(*cache), tree_u, anc, depth, gate_w, scr_c4, scr_c128,
@@ -192,8 +205,12 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
   if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
       !out || !row_status)
     return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, row_status) ||
+      (lse && !a16(lse)) || (sel && !a16(sel)))
+    return TV_ERR_INVALID_ARG;
   const WsLayout w = ws_layout(*dims);
   if (!workspace || workspace_bytes < w.total) return TV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   const tv_dims &d = *dims;
   char *ws = static_cast<char *>(workspace);
@@ -221,6 +238,9 @@ tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const ui
   if (st != TV_OK) return st;
   if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
       !accept_nodes || !accept_len || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) ||
+      !all_a16(tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes, accept_len, row_status))
     return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("commit_path", launch_commit(*dims, *cache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,

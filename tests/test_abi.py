@@ -80,3 +80,19 @@ def test_profile_capacity_checked_without_gpu():
     lib = binding.lib()
     assert lib.tv_profile_enable(0) == binding.TV_ERR_INVALID_ARG
     assert lib.tv_profile_read(None, 4, None) == binding.TV_ERR_INVALID_ARG
+
+
+def test_misaligned_pointers_rejected_without_gpu():
+    """Row buffers move with 16-byte accesses: an address off a 16-byte boundary is an argument error,
+    found on the host before any device call (the addresses are never dereferenced)."""
+    lib = binding.lib()
+    d = _dims()
+    ok, bad = ctypes.c_void_p(1 << 20), ctypes.c_void_p((1 << 20) + 8)
+    assert lib.tv_build_tree_mask(ctypes.byref(d), bad, ok, ok, ok, None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_build_tree_mask(ctypes.byref(d), ok, ok, ok, bad, None) == binding.TV_ERR_INVALID_ARG
+    cache = binding.TvCache()
+    for name, _ in binding.TvCache._fields_:
+        setattr(cache, name, ok.value)
+    cache.c4_idx = bad.value
+    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([ok] * 7), None) == \
+        binding.TV_ERR_INVALID_ARG
