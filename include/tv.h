@@ -99,7 +99,7 @@ typedef struct {
   int32_t topk;      /* CSA entries kept per node, >= 1 */
   int32_t ring_cap;  /* raw-token ring slots per row: power of two >= max(window, ratio_csa, ratio_hca) */
   int32_t max_len;   /* bound on every len[b]; sizes launches and the verify workspace */
-  float scale;       /* logit scale, normally 1/sqrt(d_k) */
+  float scale;       /* logit scale, finite and > 0, normally 1/sqrt(d_k) */
 } tv_dims;
 
 /* Committed (persistent) state of every row.  Only tv_commit_accepted_path

@@ -33,7 +33,7 @@ static tv_status check_dims(const tv_dims *dp) {
   if (d.window < 1 || d.topk < 1) return TV_ERR_INVALID_ARG;
   if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window, d.ratio_csa, d.ratio_hca})) return TV_ERR_INVALID_ARG;
   if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
-  if (!std::isfinite(d.scale)) return TV_ERR_INVALID_ARG;
+  if (!std::isfinite(d.scale) || !(d.scale > 0.f)) return TV_ERR_INVALID_ARG;
   if (d.B > 4096 || !shape_supported(d)) return TV_ERR_UNSUPPORTED;
   return TV_OK;
 }
@@ -76,7 +76,7 @@ SplitPlan split_plan(const tv_dims &d) {
   const int64_t nodes = (int64_t)d.B * d.D;
   int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (512 + nodes - 1) / nodes));
   splits = (int)std::min<int64_t>(splits, (mk + 31) / 32);
-  splits = (int)std::max<int64_t>(splits, (mk + 1535) / 1536);  // the attention kernel's pointer table bound
+  splits = (int)std::max<int64_t>(splits, (mk + kAttnMaxChunk - 1) / kAttnMaxChunk);  // pointer table bound
   int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
   p.chunk = (int32_t)chunk;
   p.splits = (int32_t)((mk + chunk - 1) / chunk);
@@ -99,6 +99,8 @@ WsLayout ws_layout(const tv_dims &d) {
   if (w.plan.splits > 1) off = align256(off + sizeof(float) * nodes * w.plan.splits * d.H * d.d_v);
   w.part_ml = off;
   if (w.plan.splits > 1) off = align256(off + sizeof(float) * 2 * nodes * w.plan.splits * d.H);
+  w.row_order = off;
+  off = align256(off + sizeof(int32_t) * d.B);
   w.total = off;
   return w;
 }
@@ -220,10 +222,11 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
   float *part_ml = reinterpret_cast<float *>(ws + w.part_ml);
   const CacheView cv = view(*cache);
   TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
+  int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
   TV_LAUNCH("topk_select", launch_topk(d, cv, anc, depth, scr_c4, q_idx, w_idx, scores, w.score_stride, selp,
-                                       row_status, stream));
-  TV_LAUNCH("verify_attn", launch_attn(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q, selp, row_status, w.plan,
-                                       part_o, part_ml, out, lse, stream));
+                                       row_status, row_order, stream));
+  TV_LAUNCH("verify_attn", launch_attn(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q, selp, row_status,
+                                       row_order, w.plan, part_o, part_ml, out, lse, stream));
   if (w.plan.splits > 1)
     TV_LAUNCH("attn_combine", launch_combine(d, cv, anc, depth, selp, row_status, w.plan, part_o, part_ml, out, lse,
                                              stream));

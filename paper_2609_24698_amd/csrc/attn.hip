@@ -31,7 +31,7 @@
 namespace tv {
 
 constexpr int kKT = 32;          // keys per tile
-constexpr int kMaxChunk = 1536;  // keys per split (pointer table in LDS)
+constexpr int kMaxChunk = kAttnMaxChunk;  // keys per split (pointer table in LDS)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -63,15 +63,18 @@ struct AttnShape {
   }
 };
 
-// Decode the XCD-aware block index: all units of row b run on XCD b % 8
-// (workgroups are dealt to the 8 XCDs round-robin), so the rows' shared HCA,
-// window and overlapping CSA entries stay in one L2.
-__device__ __forceinline__ void unit_of(int blk, int D, int splits, int &b, int &i, int &s) {
+// Decode the XCD-aware block index.  Workgroups are dealt to the 8 XCDs
+// round-robin and each XCD starts its workgroups in order, so rows are dealt
+// to XCDs in the order row_order gives (longest first): every unit of the
+// row of rank rho runs on XCD rho % 8, where the row's shared HCA, window and
+// overlapping CSA entries stay in one L2, and each XCD starts its longest
+// rows first.  Returns the rank; b is valid when the rank is below B.
+__device__ __forceinline__ int unit_of(int blk, int D, int splits, int &i, int &s) {
   const int x = blk & 7, q = blk >> 3;
   s = q % splits;
   const int r = q / splits;
   i = r % D;
-  b = (r / D) * 8 + x;
+  return (r / D) * 8 + x;
 }
 
 // Barrier that waits for this wavefront's LDS traffic only: global loads in
@@ -107,7 +110,8 @@ __global__ void __launch_bounds__(NW * 64, 1)
 attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
             const int32_t *__restrict__ depth, const uint16_t *__restrict__ scr_c4,
             const uint16_t *__restrict__ scr_c128, const uint16_t *__restrict__ q, const int32_t *__restrict__ sel,
-            const int32_t *__restrict__ row_status, int chunk, int splits, float *__restrict__ part_o,
+            const int32_t *__restrict__ row_status, const int32_t *__restrict__ row_order, int chunk, int splits,
+            float *__restrict__ part_o,
             float *__restrict__ part_ml, uint16_t *__restrict__ out, float *__restrict__ lse) {
   using S = AttnShape<NW, HT, DK, DV, VOFF, DROW>;
   constexpr int NT = NW * 64;
@@ -121,32 +125,15 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   __shared__ float sMx[HT][S::NP][32];
   __shared__ float sRef[HT][32];
 
-  int b, i, split;
-  unit_of(blockIdx.x, d.D, splits, b, i, split);
-  if (b >= d.B) return;
+  int i, split;
+  const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
+  if (rank >= d.B) return;
+  const int b = row_order[rank];
   if (row_status[b] != TV_ROW_OK) return;
-  const int32_t L = c.len[b];
-  if (!len_ok(L, d.max_len)) return;
-  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  const int k0 = split * chunk;
-  if (k0 >= nk.n_keys) return;
-  const int k1 = std::min(nk.n_keys, k0 + chunk);
-  const int nkeys = k1 - k0;
-  const int ntiles = (nkeys + kKT - 1) / kKT;
   const int64_t node = (int64_t)b * d.D + i;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int ht = wv % HT, part = wv / HT;
-
-  // key row pointers of this split
-  {
-    const int32_t *sel_node = sel + node * d.topk;
-    const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
-    for (int t = tid; t < nkeys; t += NT)
-      sPtr[t] = key_row(d, nk, b, k0 + t, sel_node, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4,
-                        scr_c128, tree_u);
-  }
-
   // This wave's logit k-steps are ks = 4m + part: channels 16 ks + 8 hi of
   // the key row (A, from LDS) and of the query (B, kept in registers).  The
   // key chunk 8m + 2 part + hi keeps its low three bits across m, so the A
@@ -162,6 +149,24 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
       qf[m] = __builtin_bit_cast(bf16x8, v);
     }
   }
+  const int32_t L = c.len[b];
+  if (!len_ok(L, d.max_len)) return;
+  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
+  const int k0 = split * chunk;
+  if (k0 >= nk.n_keys) return;
+  const int k1 = std::min(nk.n_keys, k0 + chunk);
+  const int nkeys = k1 - k0;
+  const int ntiles = (nkeys + kKT - 1) / kKT;
+
+  // key row pointers of this split
+  {
+    const int32_t *sel_node = sel + node * d.topk;
+    const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
+    for (int t = tid; t < nkeys; t += NT)
+      sPtr[t] = key_row(d, nk, b, k0 + t, sel_node, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4,
+                        scr_c128, tree_u);
+  }
+
   const int aoff = S::off(l32, (2 * part + hi) * 8);
   // Value-operand offsets for the transpose reads: rows 16 ks + 8 s + 4 hi + jj/4,
   // columns VOFF + wv*DVW + 16 (g&1) + 4 (jj&3) + 32 ct.
@@ -188,18 +193,22 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   __syncthreads();                     // pointer table ready
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
-  // Rows past the split's end re-read its last key (finite data, probability forced to 0).
-  auto issue_tile = [&](int tile, int buf) {
-    const unsigned char *src[S::NPW];
+  // Source addresses of this wave's copies of the next tile to issue, read
+  // from the pointer table one phase ahead of the copies.  Rows past the
+  // split's end re-read its last key (finite data, probability forced to 0).
+  const unsigned char *nsrc[S::NPW];
+  auto load_srcs = [&](int tile) {
 #pragma unroll
-    for (int k = 0; k < S::NPW; ++k) {  // all pointer reads first: one LDS wait
+    for (int k = 0; k < S::NPW; ++k) {
       const int t = std::min(tile * kKT + (gmap[k] & 255), nkeys - 1);
-      src[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
+      nsrc[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
     }
+  };
+  auto issue_tile = [&](int buf) {
 #pragma unroll
     for (int k = 0; k < S::NPW; ++k) {
       const int ins = wv + NW * k;
-      if (S::NINS % NW == 0 || ins < S::NINS) dma16(src[k], lds_base + buf * S::TILE_BYTES + ins * 1024);
+      if (S::NINS % NW == 0 || ins < S::NINS) dma16(nsrc[k], lds_base + buf * S::TILE_BYTES + ins * 1024);
     }
   };
   // vmcnt bound that leaves this wave's copies of the newest tile in flight
@@ -228,12 +237,21 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   // Logits of tile `it` (buffer it % 3): this wave's partial S^T, published for the reduce-scatter.
   auto qk_tile = [&](int it) {
     const unsigned char *kt = sK[it % NBUF];
+    bf16x8 a[S::KSP];
+#pragma unroll
+    for (int m = 0; m < S::KSP; ++m) a[m] = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
     f32x16 sacc = f32x16{};
 #pragma unroll
-    for (int m = 0; m < S::KSP; ++m) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[m], sacc, 0, 0, 0);
+    for (int m = 0; m < S::KSP; ++m) sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m], qf[m], sacc, 0, 0, 0);
+    // schedule: key reads kept four ahead of the products
+    constexpr int kAhead = S::KSP < 4 ? S::KSP : 4;
+    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+    for (int r = 0; r < S::KSP - kAhead; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
     float4 *mine = reinterpret_cast<float4 *>(&sX[ht][part][lane][0]);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
@@ -243,14 +261,17 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   // sum the four partials in part order, exponentiate against the reference,
   // publish bf16 P and the overflow flag.
   auto softmax_tile = [&](int it, bool set_ref) {
-    float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 t4[S::NP];
 #pragma unroll
-    for (int p = 0; p < S::NP; ++p) {
-      const float4 t4 = reinterpret_cast<const float4 *>(&sX[ht][p][lane][0])[part ^ xsw];
-      s4.x += t4.x;
-      s4.y += t4.y;
-      s4.z += t4.z;
-      s4.w += t4.w;
+    for (int p = 0; p < S::NP; ++p) t4[p] = reinterpret_cast<const float4 *>(&sX[ht][p][lane][0])[part ^ xsw];
+    __builtin_amdgcn_sched_group_barrier(0x100, S::NP, 0);  // the partials in flight together
+    float4 s4 = t4[0];
+#pragma unroll
+    for (int p = 1; p < S::NP; ++p) {
+      s4.x += t4[p].x;
+      s4.y += t4[p].y;
+      s4.z += t4[p].z;
+      s4.w += t4[p].w;
     }
     float sv[4] = {s4.x, s4.y, s4.z, s4.w};
     const int nvalid = nkeys - it * kKT;
@@ -259,11 +280,11 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
       for (int r = 0; r < 4; ++r)
         if (8 * part + 4 * hi + r >= nvalid) sv[r] = -INFINITY;
     }
-    float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
+    const float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])) * sl2;  // this lane's four rows
     m_seen = fmaxf(m_seen, mloc);
     if (set_ref) {  // the reference is the first tile's maximum over all four quarters
-      if (hi == 0) sMx[ht][part][l32] = mloc;
+      const float mh = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      if (hi == 0) sMx[ht][part][l32] = mh;
       lds_barrier();
       m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
     }
@@ -304,10 +325,14 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
       }
     }
   };
-  // Tile t+2 copy issue and the wait for tile t+1 (Y phase of tile t).
-  auto advance = [&](int t) {
+  // Y phase of tile t: copy of tile t+2 into the buffer of tile t-1 (read by
+  // every wave before this phase), then, after the probabilities, the wait
+  // for tile t+1.
+  auto issue_next = [&](int t) {
+    if (t + 2 < ntiles) issue_tile((t + 2) % NBUF);
+  };
+  auto wait_next = [&](int t) {
     if (t + 2 < ntiles) {
-      issue_tile(t + 2, (t + 2) % NBUF);  // buffer of tile t-1, read by every wave before this phase
       if (full_share)
         vm_wait<S::NPW>();
       else
@@ -329,38 +354,50 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
     l_run = 0.f;
     const bool first = attempt == 0;
     bool restart = false;
-    issue_tile(0, 0);
-    if (ntiles > 1) issue_tile(1, 1);
+    load_srcs(0);
+    issue_tile(0);
+    if (ntiles > 1) {
+      load_srcs(1);
+      issue_tile(1);
+    }
+    if (ntiles > 2) load_srcs(2);
     vm_wait<0>();
     __syncthreads();
     qk_tile(0);
     lds_barrier();
+    issue_next(0);
     softmax_tile(0, first);
-    advance(0);
+    wait_next(0);
     lds_barrier();
 
     for (int it = 0; it < ntiles; ++it) {
       const bool more = it + 1 < ntiles;
-      pv_tile(it);
-      if (more) qk_tile(it + 1);
-      int anyf = 0;
+      // X phase: logits of tile it+1 first (their partials are published at
+      // the end of the phase), then P V of tile it, whose products may still
+      // be in the matrix pipeline during the next phase.
+      int anyf = 0;  // overflow flags of the probabilities of tile it
 #pragma unroll
       for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
+      if (it + 3 < ntiles) load_srcs(it + 3);  // copied in the next phase
+      if (more) qk_tile(it + 1);
+      pv_tile(it);
       if (anyf) {  // probabilities of tile it overflowed the reference
         restart = attempt < kMaxRestarts;
         if (restart) break;
       }
       if (!more) break;
       lds_barrier();
+      issue_next(it + 1);
       softmax_tile(it + 1, false);
-      advance(it + 1);
+      wait_next(it + 1);
       lds_barrier();
     }
     if (!restart) break;
     // restart from the largest logit any quarter has seen, agreed through LDS
     vm_wait<0>();
     __syncthreads();
-    if (hi == 0) sMx[ht][part][l32] = m_seen;
+    const float ms = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));
+    if (hi == 0) sMx[ht][part][l32] = ms;
     __syncthreads();
     m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
     __syncthreads();
@@ -469,26 +506,27 @@ template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 static hipError_t launch_attn_t(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                                 const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                                 const uint16_t *q, const int32_t *sel, const int32_t *row_status,
-                                const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
-                                hipStream_t s) {
+                                const int32_t *row_order, const SplitPlan &plan, float *part_o, float *part_ml,
+                                uint16_t *out, float *lse, hipStream_t s) {
   if (plan.chunk > kMaxChunk) return hipErrorInvalidValue;
   const int64_t grid = (int64_t)((d.B + 7) / 8) * 8 * d.D * plan.splits;
   attn_kernel<NW, HT, DK, DV, VOFF, DROW><<<dim3((unsigned)grid), NW * 64, 0, s>>>(
-      d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status, plan.chunk, plan.splits, part_o, part_ml,
-      out, lse);
+      d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status, row_order, plan.chunk, plan.splits, part_o,
+      part_ml, out, lse);
   return hipGetLastError();
 }
 
 hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
-                       const int32_t *sel, const int32_t *row_status, const SplitPlan &plan, float *part_o,
-                       float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
+                       const int32_t *sel, const int32_t *row_status, const int32_t *row_order,
+                       const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
+                       hipStream_t s) {
   if (d.H == 64 && d.d_k == 576 && d.d_v == 512 && d.v_off == 0 && d.d_row == 576)
     return launch_attn_t<8, 2, 576, 512, 0, 576>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
-                                                 plan, part_o, part_ml, out, lse, s);
+                                                 row_order, plan, part_o, part_ml, out, lse, s);
   if (d.H == 8 && d.d_k == 128 && d.d_v == 128 && d.v_off == 128 && d.d_row == 256)
     return launch_attn_t<4, 1, 128, 128, 128, 256>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
-                                                   plan, part_o, part_ml, out, lse, s);
+                                                   row_order, plan, part_o, part_ml, out, lse, s);
   return hipErrorInvalidValue;
 }
 

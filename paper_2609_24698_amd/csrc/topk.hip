@@ -46,7 +46,8 @@ __global__ void __launch_bounds__(kNT) topk_kernel(tv_dims d, CacheView c, const
                                                    const uint16_t *__restrict__ q_idx,
                                                    const uint16_t *__restrict__ w_idx,
                                                    const float *__restrict__ scores, int score_stride,
-                                                   int32_t *__restrict__ sel, int32_t *__restrict__ row_status) {
+                                                   int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
+                                                   int32_t *__restrict__ row_order) {
   __shared__ __align__(16) uint32_t keys[kLds ? kLdsKeys : 4];
   __shared__ __align__(16) uint32_t hist[256 * kCopies];
   __shared__ float scr_score[kMaxScratch];
@@ -57,6 +58,26 @@ __global__ void __launch_bounds__(kNT) topk_kernel(tv_dims d, CacheView c, const
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int b = blockIdx.x / d.D;
   const int i = blockIdx.x - b * d.D;
+  if (i == 0) {
+    // Rank of row b by (committed length descending, row ascending), for every
+    // row whatever its status: row_order[rank] = b.  The attention kernel
+    // starts the longest rows first.
+    const int32_t Lb = c.len[b];
+    int cnt = 0;
+    for (int r = tid; r < d.B; r += kNT) {
+      const int32_t Lr = c.len[r];
+      cnt += (Lr > Lb || (Lr == Lb && r < b)) ? 1 : 0;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    if (lane == 0) wcnt[1][wv] = cnt;
+    __syncthreads();
+    if (tid == 0) {
+      int rank = 0;
+      for (int w = 0; w < kNW; ++w) rank += wcnt[1][w];
+      row_order[rank] = b;
+    }
+  }
   if (row_status[b] != TV_ROW_OK) return;
   const int32_t L = c.len[b];
   if (!len_ok(L, d.max_len)) {
@@ -342,16 +363,17 @@ __global__ void __launch_bounds__(kNT) topk_kernel(tv_dims d, CacheView c, const
 
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                        const uint16_t *scr_c4, const uint16_t *q_idx, const uint16_t *w_idx, const float *scores,
-                       int32_t score_stride, int32_t *sel, int32_t *row_status, hipStream_t s) {
+                       int32_t score_stride, int32_t *sel, int32_t *row_status, int32_t *row_order,
+                       hipStream_t s) {
   if (d.D > kMaxScratch) return hipErrorInvalidValue;
   // the LDS variant serves every node when the longest candidate list fits
   const int64_t max_n = (int64_t)d.max_len / d.ratio_csa + d.D;
   if (max_n <= kLdsKeys)
     topk_kernel<true><<<d.B * d.D, kNT, 0, s>>>(d, c, anc, depth, scr_c4, q_idx, w_idx, scores, score_stride, sel,
-                                                row_status);
+                                                row_status, row_order);
   else
     topk_kernel<false><<<d.B * d.D, kNT, 0, s>>>(d, c, anc, depth, scr_c4, q_idx, w_idx, scores, score_stride, sel,
-                                                 row_status);
+                                                 row_status, row_order);
   return hipGetLastError();
 }
 

@@ -17,6 +17,9 @@ struct CacheView {
   const int32_t *len;
 };
 
+// Keys one attention workgroup takes per split (its LDS pointer table).
+constexpr int kAttnMaxChunk = 1280;
+
 // How the verify attention splits a node's keys across workgroups.
 struct SplitPlan {
   int32_t max_keys;   // upper bound of any node's key count
@@ -30,6 +33,7 @@ struct WsLayout {
   size_t sel;         // int32 [B*D][topk], used when the caller passes no sel
   size_t part_o;      // float [B*D][splits][H][d_v]
   size_t part_ml;     // float2 [B*D][splits][H] (running max in log2 units, sum)
+  size_t row_order;   // int32 [B]: rows by committed length, longest first
   size_t total;
   int32_t score_stride;
   SplitPlan plan;
@@ -47,11 +51,12 @@ hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_
                         const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s);
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                        const uint16_t *scr_c4, const uint16_t *q_idx, const uint16_t *w_idx, const float *scores,
-                       int32_t score_stride, int32_t *sel, int32_t *row_status, hipStream_t s);
+                       int32_t score_stride, int32_t *sel, int32_t *row_status, int32_t *row_order, hipStream_t s);
 hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
-                       const int32_t *sel, const int32_t *row_status, const SplitPlan &plan, float *part_o,
-                       float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+                       const int32_t *sel, const int32_t *row_status, const int32_t *row_order,
+                       const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
+                       hipStream_t s);
 hipError_t launch_combine(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                           const int32_t *sel, const int32_t *row_status, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s);
