@@ -101,6 +101,10 @@ WsLayout ws_layout(const tv_dims &d) {
   if (w.plan.splits > 1) off = align256(off + sizeof(float) * 2 * nodes * w.plan.splits * d.H);
   w.row_order = off;
   off = align256(off + sizeof(int32_t) * d.B);
+  w.keytab = off;
+  off = align256(off + sizeof(void *) * nodes * w.plan.max_keys);
+  w.nkeys = off;
+  off = align256(off + sizeof(int32_t) * nodes);
   w.total = off;
   return w;
 }
@@ -223,13 +227,15 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
   const CacheView cv = view(*cache);
   TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
   int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
-  TV_LAUNCH("topk_select", launch_topk(d, cv, anc, depth, scr_c4, q_idx, w_idx, scores, w.score_stride, selp,
-                                       row_status, row_order, stream));
-  TV_LAUNCH("verify_attn", launch_attn(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q, selp, row_status,
-                                       row_order, w.plan, part_o, part_ml, out, lse, stream));
+  const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
+  int32_t *nkeys = reinterpret_cast<int32_t *>(ws + w.nkeys);
+  TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
+                                       w.score_stride, selp, row_status, row_order, keytab, w.plan.max_keys, nkeys,
+                                       stream));
+  TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys, w.plan, part_o, part_ml, out, lse,
+                                       stream));
   if (w.plan.splits > 1)
-    TV_LAUNCH("attn_combine", launch_combine(d, cv, anc, depth, selp, row_status, w.plan, part_o, part_ml, out, lse,
-                                             stream));
+    TV_LAUNCH("attn_combine", launch_combine(d, row_status, nkeys, w.plan, part_o, part_ml, out, lse, stream));
   return TV_OK;
 }
 

@@ -24,7 +24,6 @@
 // combine kernel merges in split order.
 #include <algorithm>
 
-#include "node_keys.h"
 #include "tv_common.h"
 #include "tv_internal.h"
 
@@ -107,11 +106,9 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 __global__ void __launch_bounds__(NW * 64, 1)
-attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
-            const int32_t *__restrict__ depth, const uint16_t *__restrict__ scr_c4,
-            const uint16_t *__restrict__ scr_c128, const uint16_t *__restrict__ q, const int32_t *__restrict__ sel,
-            const int32_t *__restrict__ row_status, const int32_t *__restrict__ row_order, int chunk, int splits,
-            float *__restrict__ part_o,
+attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict__ row_status,
+            const int32_t *__restrict__ row_order, const uint16_t *const *__restrict__ keytab, int keytab_stride,
+            const int32_t *__restrict__ nkeys_tab, int chunk, int splits, float *__restrict__ part_o,
             float *__restrict__ part_ml, uint16_t *__restrict__ out, float *__restrict__ lse) {
   using S = AttnShape<NW, HT, DK, DV, VOFF, DROW>;
   constexpr int NT = NW * 64;
@@ -119,7 +116,6 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   __shared__ __attribute__((aligned(1024))) unsigned char sK[NBUF][S::TILE_BYTES];
   __shared__ __attribute__((aligned(16))) float sX[HT][S::NP][64][16];
   __shared__ const uint16_t *sPtr[kMaxChunk];
-  __shared__ int32_t path[64], hca_node[64], cnt[2];
   __shared__ int sFlag[NW];
   __shared__ uint2 sP[HT][S::NP][64];
   __shared__ float sMx[HT][S::NP][32];
@@ -129,11 +125,27 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
   const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
   if (rank >= d.B) return;
   const int b = row_order[rank];
-  if (row_status[b] != TV_ROW_OK) return;
   const int64_t node = (int64_t)b * d.D + i;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int ht = wv % HT, part = wv / HT;
+  const int k0 = split * chunk;
+  // Everything the prologue needs is loaded at once: row status, key count,
+  // this thread's entries of the node's key table (the top-k kernel wrote it;
+  // entries past the count are never used) and the queries.  The table loads
+  // come first so that storing them waits for them only.
+  const int32_t status = row_status[b];
+  const int n_keys = nkeys_tab[node];
+  constexpr int kPer = (kMaxChunk + NT - 1) / NT;
+  const uint16_t *tp[kPer];
+  {
+    const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int t = tid + NT * u;
+      tp[u] = (t < chunk && k0 + t < keytab_stride) ? tab[t] : nullptr;
+    }
+  }
   // This wave's logit k-steps are ks = 4m + part: channels 16 ks + 8 hi of
   // the key row (A, from LDS) and of the query (B, kept in registers).  The
   // key chunk 8m + 2 part + hi keeps its low three bits across m, so the A
@@ -149,22 +161,14 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
       qf[m] = __builtin_bit_cast(bf16x8, v);
     }
   }
-  const int32_t L = c.len[b];
-  if (!len_ok(L, d.max_len)) return;
-  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  const int k0 = split * chunk;
-  if (k0 >= nk.n_keys) return;
-  const int k1 = std::min(nk.n_keys, k0 + chunk);
+  if (status != TV_ROW_OK || k0 >= n_keys) return;
+  const int k1 = std::min(n_keys, k0 + chunk);
   const int nkeys = k1 - k0;
   const int ntiles = (nkeys + kKT - 1) / kKT;
-
-  // key row pointers of this split
-  {
-    const int32_t *sel_node = sel + node * d.topk;
-    const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
-    for (int t = tid; t < nkeys; t += NT)
-      sPtr[t] = key_row(d, nk, b, k0 + t, sel_node, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4,
-                        scr_c128, tree_u);
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int t = tid + NT * u;
+    if (t < nkeys) sPtr[t] = tp[u];
   }
 
   const int aoff = S::off(l32, (2 * part + hi) * 8);
@@ -420,7 +424,7 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
 
   // epilogue: lane holds, per head tile t, head t*32 + l32 and value rows
   // wv*DVW + 32ct + 8(j/4) + 4hi + (j%4)
-  const bool single = nk.n_keys <= chunk;
+  const bool single = n_keys <= chunk;
 #pragma unroll
   for (int t = 0; t < HT; ++t) {
     const int h = t * 32 + l32;
@@ -456,22 +460,18 @@ attn_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const u
 
 // Merge the partials of nodes whose keys spanned several splits.
 template <int DV>
-__global__ void __launch_bounds__(256) combine_kernel(tv_dims d, CacheView c, const uint64_t *__restrict__ anc,
-                                                      const int32_t *__restrict__ depth,
-                                                      const int32_t *__restrict__ row_status, int chunk, int splits,
+__global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *__restrict__ row_status,
+                                                      const int32_t *__restrict__ nkeys_tab, int chunk, int splits,
                                                       const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml, uint16_t *__restrict__ out,
                                                       float *__restrict__ lse) {
-  __shared__ int32_t path[64], hca_node[64], cnt[2];
   __shared__ float sW[64][64];  // per (split, head) weight exp2(m_s - m*) / l*
   const int nodeg = blockIdx.x;
-  const int b = nodeg / d.D, i = nodeg - b * d.D;
+  const int b = nodeg / d.D;
   if (row_status[b] != TV_ROW_OK) return;
-  const int32_t L = c.len[b];
-  if (!len_ok(L, d.max_len)) return;
-  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  if (nk.n_keys <= chunk) return;
-  const int used = (nk.n_keys + chunk - 1) / chunk;
+  const int n_keys = nkeys_tab[nodeg];
+  if (n_keys <= chunk) return;
+  const int used = (n_keys + chunk - 1) / chunk;
   const int64_t node = nodeg;
   const int tid = threadIdx.x;
   for (int h0 = 0; h0 < d.H; h0 += 64) {
@@ -503,45 +503,39 @@ __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, CacheView c, co
 }
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
-static hipError_t launch_attn_t(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
-                                const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
-                                const uint16_t *q, const int32_t *sel, const int32_t *row_status,
-                                const int32_t *row_order, const SplitPlan &plan, float *part_o, float *part_ml,
-                                uint16_t *out, float *lse, hipStream_t s) {
+static hipError_t launch_attn_t(const tv_dims &d, const uint16_t *q, const int32_t *row_status,
+                                const int32_t *row_order, const uint16_t *const *keytab, const int32_t *nkeys,
+                                const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
+                                hipStream_t s) {
   if (plan.chunk > kMaxChunk) return hipErrorInvalidValue;
   const int64_t grid = (int64_t)((d.B + 7) / 8) * 8 * d.D * plan.splits;
   attn_kernel<NW, HT, DK, DV, VOFF, DROW><<<dim3((unsigned)grid), NW * 64, 0, s>>>(
-      d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status, row_order, plan.chunk, plan.splits, part_o,
-      part_ml, out, lse);
+      d, q, row_status, row_order, keytab, plan.max_keys, nkeys, plan.chunk, plan.splits, part_o, part_ml, out, lse);
   return hipGetLastError();
 }
 
-hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
-                       const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
-                       const int32_t *sel, const int32_t *row_status, const int32_t *row_order,
-                       const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
-                       hipStream_t s) {
+hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
+                       const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
+                       float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
   if (d.H == 64 && d.d_k == 576 && d.d_v == 512 && d.v_off == 0 && d.d_row == 576)
-    return launch_attn_t<8, 2, 576, 512, 0, 576>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
-                                                 row_order, plan, part_o, part_ml, out, lse, s);
+    return launch_attn_t<8, 2, 576, 512, 0, 576>(d, q, row_status, row_order, keytab, nkeys, plan, part_o, part_ml,
+                                                 out, lse, s);
   if (d.H == 8 && d.d_k == 128 && d.d_v == 128 && d.v_off == 128 && d.d_row == 256)
-    return launch_attn_t<4, 1, 128, 128, 128, 256>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q, sel, row_status,
-                                                   row_order, plan, part_o, part_ml, out, lse, s);
+    return launch_attn_t<4, 1, 128, 128, 128, 256>(d, q, row_status, row_order, keytab, nkeys, plan, part_o,
+                                                   part_ml, out, lse, s);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_combine(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
-                          const int32_t *sel, const int32_t *row_status, const SplitPlan &plan,
+hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
-  (void)sel;
   if (plan.splits <= 1) return hipSuccess;
   dim3 grid(d.B * d.D);
   if (d.d_v == 512)
-    combine_kernel<512><<<grid, 256, 0, s>>>(d, c, anc, depth, row_status, plan.chunk, plan.splits, part_o, part_ml,
-                                             out, lse);
+    combine_kernel<512><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
+                                             lse);
   else
-    combine_kernel<128><<<grid, 256, 0, s>>>(d, c, anc, depth, row_status, plan.chunk, plan.splits, part_o, part_ml,
-                                             out, lse);
+    combine_kernel<128><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
+                                             lse);
   return hipGetLastError();
 }
 

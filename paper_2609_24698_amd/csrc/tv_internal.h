@@ -34,6 +34,8 @@ struct WsLayout {
   size_t part_o;      // float [B*D][splits][H][d_v]
   size_t part_ml;     // float2 [B*D][splits][H] (running max in log2 units, sum)
   size_t row_order;   // int32 [B]: rows by committed length, longest first
+  size_t keytab;      // const uint16_t* [B*D][plan.max_keys]: latent row of every key of every node
+  size_t nkeys;       // int32 [B*D]: key count of every node
   size_t total;
   int32_t score_stride;
   SplitPlan plan;
@@ -49,16 +51,15 @@ hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t 
                            int32_t *row_status, hipStream_t s);
 hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
                         const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s);
-hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
-                       const uint16_t *scr_c4, const uint16_t *q_idx, const uint16_t *w_idx, const float *scores,
-                       int32_t score_stride, int32_t *sel, int32_t *row_status, int32_t *row_order, hipStream_t s);
-hipError_t launch_attn(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
-                       const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
-                       const int32_t *sel, const int32_t *row_status, const int32_t *row_order,
-                       const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
-                       hipStream_t s);
-hipError_t launch_combine(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
-                          const int32_t *sel, const int32_t *row_status, const SplitPlan &plan,
+hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
+                       const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
+                       const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
+                       int32_t *row_status, int32_t *row_order, const uint16_t **keytab, int32_t keytab_stride,
+                       int32_t *nkeys, hipStream_t s);
+hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
+                       const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
+                       float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s);
 hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
                          const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
