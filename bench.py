@@ -128,6 +128,16 @@ def cpu_baseline(wl, budget_s: float):
                        f"numpy oracle, {dt:.1f} s")
 
 
+def bench_workload(config: str, steps: int, warmup: int, seed=None):
+    """The workload the benchmark times: pools and the length bound leave room
+    for every step's commit (at most D tokens per row per step)."""
+    import synth
+
+    grow = (2 * steps + warmup + 2) * synth.CONFIGS[config]["D"]
+    return synth.make_workload(config, seed=seed, max_len_margin=grow, extra_c4=grow // 4 + 8,
+                               extra_c128=grow // 128 + 4)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,10 +173,7 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 5}))
         return
     K, W = args.steps, args.warmup
-    D_cfg = synth.CONFIGS[args.config]["D"]
-    grow = (2 * K + W + 2) * D_cfg
-    wl = synth.make_workload(args.config, seed=args.seed, max_len_margin=grow,
-                             extra_c4=grow // 4 + 8, extra_c128=grow // 128 + 4)
+    wl = bench_workload(args.config, K, W, args.seed)
     dims = wl.dims
     print(f"[bench] {args.config}: B={wl.B} D={wl.D} mean L={wl.lens.mean():.0f} "
           f"input {wl.nbytes() / 1e6:.0f} MB", file=sys.stderr, flush=True)

@@ -211,12 +211,17 @@ def indexer_scores(keys, q_idx, w_idx):
     return np.maximum(keys @ q_idx.T, 0.0) @ w_idx
 
 
-def verify_node(wl, b, i, anc, depth, scr_c4, scr_c128, rc=None):
+def verify_node(wl, b, i, anc, depth, scr_c4, scr_c128, rc=None, chosen=None):
     """Output of node i of row b: the definition written out for one query.
 
     Returns a dict with ``out`` [H][d_v], ``lse`` [H], ``sel`` (selected CSA
     logical indices, ascending), ``scores`` (logical index -> indexer score of
     every candidate) and ``n_keys`` (size of the attended key set).
+
+    ``chosen`` replaces the top-k by a given set of candidate indices.  Where
+    scores tie at the selection boundary several sets are correct; the
+    attention over a set another implementation chose is then computed with
+    that set (every index must be a visible candidate).
     """
     d = wl.dims
     r4, r128, W, k = d["ratio_csa"], d["ratio_hca"], d["window"], d["topk"]
@@ -241,8 +246,12 @@ def verify_node(wl, b, i, anc, depth, scr_c4, scr_c128, rc=None):
     cand_idx = np.asarray(cand_idx, dtype=np.int64)
     keys = np.concatenate(cand_keys, axis=0) if len(cand_idx) else np.zeros((0, d["d_idx"]))
     S = indexer_scores(keys, bf16_to_f64(wl.q_idx[b, i]), bf16_to_f64(wl.w_idx[b, i]))
-    order = np.lexsort((cand_idx, -S))  # score descending, then index ascending
-    chosen = np.sort(cand_idx[order[:min(k, len(cand_idx))]])
+    if chosen is None:
+        order = np.lexsort((cand_idx, -S))  # score descending, then index ascending
+        chosen = np.sort(cand_idx[order[:min(k, len(cand_idx))]])
+    else:
+        chosen = np.sort(np.asarray(chosen, dtype=np.int64))
+        assert len(chosen) == min(k, len(cand_idx)) and set(chosen.tolist()) <= set(cand_idx.tolist())
 
     rows = []
     for s in chosen:

@@ -53,13 +53,17 @@ def selection_matches(gpu_sel: np.ndarray, ref_detail: dict, k: int):
     return False
 
 
-def compare_verify(gpu_out, gpu_lse, gpu_sel, ref, nodes, dims, n4_rows=None):
+def compare_verify(gpu_out, gpu_lse, gpu_sel, ref, nodes, dims, n4_rows=None, rerun=None):
     """Compare verify outputs node by node; returns stats.
 
     ``n4_rows`` (committed CSA entries per row) is given when the GPU verified
     against its own scratch entries rather than the oracle's: those may differ
     from the oracle's in the last bfloat16 bit, which may move a scratch
     candidate across the selection boundary; such nodes are counted, not failed.
+    ``rerun(b, i, chosen)`` returns the oracle's result for a node with a given
+    selection; when it is given, nodes whose selection legitimately differs
+    (near ties, scratch entries) are compared against the oracle run on the
+    GPU's selection instead of being skipped.
     """
     k = dims["topk"]
     ties = scratch = 0
@@ -75,12 +79,14 @@ def compare_verify(gpu_out, gpu_lse, gpu_sel, ref, nodes, dims, n4_rows=None):
             if any(s >= n4_rows[b] for s in diff):
                 m = "scratch"
         assert m is not False, f"selection mismatch at row {b} node {i}"
-        if m == "tie":
-            ties += 1
-            continue
-        if m == "scratch":
-            scratch += 1
-            continue
+        if m == "tie" or m == "scratch":
+            if m == "tie":
+                ties += 1
+            else:
+                scratch += 1
+            if rerun is None:
+                continue
+            det = rerun(b, i, gpu_sel[b, i][gpu_sel[b, i] >= 0])
         mx, mean = bf16_err(gpu_out[b, i], det["out"])
         assert mx <= MAX_ABS, f"out row {b} node {i}: max-abs {mx:.3e}"
         worst = max(worst, mx)

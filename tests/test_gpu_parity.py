@@ -38,7 +38,15 @@ def _round(case):
     return w, ref, r
 
 
-def _check_stages(w, ref, r, nodes=None):
+def _rerun(w, ref):
+    """The oracle's result for a node on a given selection (for nodes where
+    several selections are correct)."""
+    def f(b, i, chosen):
+        return O.verify_node(w, b, i, ref["anc"], ref["depth"], ref["scr_c4"], ref["scr_c128"], chosen=chosen)
+    return f
+
+
+def _check_stages(w, ref, r, nodes=None, rerun=None):
     d = w.dims
     B, D = w.B, w.D
     # verify preprocess
@@ -67,7 +75,8 @@ def _check_stages(w, ref, r, nodes=None):
     ok_nodes = [(b, i) for b in range(B) for i in range(D) if ref["status_verify"][b] == 0]
     if nodes is not None:
         ok_nodes = [n for n in nodes if n in ref["detail"]]
-    stats = compare_verify(r.host("out"), r.host("lse"), r.host("sel"), ref, ok_nodes, d)
+    stats = compare_verify(r.host("out"), r.host("lse"), r.host("sel"), ref, ok_nodes, d,
+                           rerun=rerun if rerun is not None else _rerun(w, ref))
     _say(f"  verify {stats}")
     bad_rows = [b for b in range(B) if ref["status_verify"][b] != 0]
     for b in bad_rows:  # skipped rows keep their poisoned outputs

@@ -1,0 +1,158 @@
+"""GPU parity at full workload sizes, on error rows, and for the variants the
+small cases do not reach.
+
+Full sizes run in the benchmark's launch configuration (its workload, its
+length bound, hence its split plan) and compare every stage on sampled nodes
+the oracle computes one by one: masks, commit layout and row status over all
+rows, compressed entries over all closing nodes, verify outputs on the
+sampled nodes.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import bench
+import synth
+from oracle import tv_oracle as O
+
+from .parity import assert_bf16_close, compare_verify
+from .test_gpu_parity import _check_stages
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _rerun(w, ref):
+    def f(b, i, chosen):
+        return O.verify_node(w, b, i, ref["anc"], ref["depth"], ref["scr_c4"], ref["scr_c128"], chosen=chosen)
+    return f
+
+
+def _device(w):
+    from paper_2609_24698_amd import DeviceRound
+    return DeviceRound(w, "cuda:0")
+
+
+def _full(config, rows, chain=False):
+    if chain:
+        w = synth.make_workload(config, chain=True)
+    else:
+        w = bench.bench_workload(config, 20, 5)
+    rows = sorted(set(int(b) for b in rows))
+    nodes = [(b, i) for b in rows for i in range(w.D)]
+    _say(f"[workload] {config} chain={chain} B={w.B} D={w.D} rows={rows} lens={[int(w.lens[b]) for b in rows]}")
+    ref = O.run_round(w, nodes)
+    r = _device(w)
+    stats = _check_stages(w, ref, r, nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
+    return stats
+
+
+def test_c2_tree_full_size():
+    _full("C2", [0, 13, 31])
+
+
+def test_c2_chain_twin_full_size():
+    """The chain twin of the B=32 workload: identical bytes, parents [-1, 0, 1, ...]."""
+    _full("C2", [0, 31], chain=True)
+
+
+def test_c3_full_size():
+    w = bench.bench_workload("C3", 20, 5)
+    order = np.argsort(w.lens)
+    # the longest and shortest rows, rows whose tree closes an HCA block, one more
+    rows = [order[-1], order[-2], order[0], 0, 1, 2, 3, 40]
+    _full("C3", rows)
+
+
+def test_c4_full_size():
+    """One row of 1M committed tokens: 262,144 indexer candidates per node
+    (the global-memory top-k path) and split attention with the combine."""
+    _full("C4", [0])
+
+
+def _small(B=5, D=8, lens=(1003, 2047, 999, 1023, 1500), seed=71, **over):
+    return synth.make_workload("C1", B=B, D=D, lens=list(lens), seed=seed, topk=64, **over)
+
+
+def test_row_errors():
+    """A bad parent array, an accepted node outside the tree, a pool too small
+    for the path's new entry and a length beyond the bound each fail their own
+    row only; the row keeps its cache and its outputs stay unwritten."""
+    w = _small()
+    assert (int(w.lens[3]) + 1) % 4 == 0  # the root of row 3 closes a CSA block
+    w.parents[1, 3] = 5                   # parent after the node
+    w.accepted_last[2] = w.D              # outside the tree
+    w.c4_cap[3] = int(w.lens[3]) // 4     # no slot for the entry the root closes
+    w.lens[4] = w.dims["max_len"] + 1     # beyond the bound
+    ref = O.run_round(w)
+    assert list(ref["commit"]["status"]) == [O.ROW_OK, O.ROW_BAD_PARENT, O.ROW_BAD_ACCEPT, O.ROW_CAPACITY,
+                                             O.ROW_BAD_LEN]
+    r = _device(w)
+    _check_stages(w, ref, r, rerun=_rerun(w, ref))
+
+
+def test_deterministic():
+    """Two launches on the same inputs give the same bits (fixed reduction orders)."""
+    w = _small(seed=72)
+    r = _device(w)
+    r.mask()
+    r.compress()
+    r.verify()
+    torch.cuda.synchronize()
+    first = {k: r.host(k).copy() for k in ("scr_c4", "scr_c128", "out", "lse", "sel")}
+    r.verify()
+    r.compress()
+    r.verify()
+    torch.cuda.synchronize()
+    for k, v in first.items():
+        assert np.array_equal(r.host(k).view(np.uint8), v.view(np.uint8)), k
+
+
+@pytest.mark.parametrize("over", [dict(H_idx=1), dict(H_idx=64), dict(D=16), dict(D=16, H_idx=4)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_indexer_variants(over):
+    """Indexer head counts and tree sizes served by the general scoring kernel."""
+    D = over.pop("D", 8)
+    w = _small(B=3, D=D, lens=(1003, 4095, 2046), seed=73, **over)
+    ref = O.run_round(w)
+    r = _device(w)
+    _check_stages(w, ref, r, rerun=_rerun(w, ref))
+
+
+def test_round_on_own_scratch():
+    """The whole round on the GPU's own intermediates: verify reads the GPU's
+    scratch entries (which may differ from the oracle's in the last bit) and
+    commit stores them."""
+    w = _small(B=4, lens=(1003, 2047, 1023, 3071), seed=74)
+    ref = O.run_round(w)
+    r = _device(w)
+    r.round()
+    torch.cuda.synchronize()
+    d = w.dims
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    n4_rows = [int(L) // d["ratio_csa"] for L in w.lens]
+
+    def rerun_own(b, i, chosen):
+        g4, g128 = r.host("scr_c4"), r.host("scr_c128")
+        return O.verify_node(w, b, i, ref["anc"], ref["depth"], g4, g128, chosen=chosen)
+
+    stats = compare_verify(r.host("out"), r.host("lse"), r.host("sel"), ref, nodes, d, n4_rows=n4_rows,
+                           rerun=rerun_own)
+    _say(f"  own scratch: {stats}")
+    com = ref["commit"]
+    assert np.array_equal(r.host("len"), com["lens"])
+    assert np.array_equal(r.host("ring"), com["ring"])
+    assert np.array_equal(r.host("accept_len"), com["accept_len"])
+    assert np.array_equal(r.host("accept_nodes"), com["accept_nodes"])
+    for name in ("c4", "c4_idx", "c128"):
+        g, o = r.host(name), com[name]
+        diff = np.any(g != o, axis=-1)
+        if diff.any():  # only entries the path closed, within the bfloat16 tolerance
+            assert_bf16_close(g[diff], O.bf16_to_f64(o[diff]), f"committed {name} entries")
