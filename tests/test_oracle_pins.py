@@ -407,3 +407,39 @@ def test_len_beyond_bound_is_flagged():
     w.dims["max_len"] = 300
     res = O.run_round(w)
     assert list(res["status_verify"]) == [O.ROW_OK, O.ROW_BAD_LEN]
+
+
+def test_given_selection_replaces_only_the_csa_rows():
+    """A given selection reproduces the node exactly when it is the top-k
+    itself; swapping one chosen entry for an unchosen one changes exactly one
+    attended CSA row (the committed entry's row), checked against SDPA over
+    the explicitly gathered keys."""
+    w = synth.make_workload("C0", lens=1500, topk=32, seed=12)
+    anc, depth, st = O.build_tree_mask(w.parents)
+    scr4, scr128, *_ = O.branch_compress(w, anc, depth, st)
+    d = w.dims
+    base = O.verify_node(w, 0, 3, anc, depth, scr4, scr128)
+    same = O.verify_node(w, 0, 3, anc, depth, scr4, scr128, chosen=base["sel"])
+    assert np.array_equal(same["out"], base["out"]) and np.array_equal(same["sel"], base["sel"])
+    unchosen = sorted(set(base["scores"]) - set(base["sel"].tolist()))
+    swapped = np.sort(np.concatenate([base["sel"][1:], [unchosen[0]]]))
+    alt = O.verify_node(w, 0, 3, anc, depth, scr4, scr128, chosen=swapped)
+    assert np.array_equal(alt["sel"], swapped) and alt["n_keys"] == base["n_keys"]
+    assert not np.allclose(alt["out"], base["out"])
+    # brute force on the swapped set: committed CSA rows of the set, every HCA
+    # entry, the window (committed ring rows and the root path's draft rows)
+    n4 = int(w.lens[0]) // d["ratio_csa"]
+    assert all(s < n4 for s in swapped)  # node 3 closes no block at this length
+    rows = [O.bf16_to_f64(w.c4[w.c4_base[0] + s]) for s in swapped]
+    rows += [O.bf16_to_f64(w.c128[w.c128_base[0] + s]) for s in range(int(w.lens[0]) // d["ratio_hca"])]
+    path = O.node_path(anc[0], depth[0], 3)
+    L, p = int(w.lens[0]), int(w.lens[0]) + int(depth[0, 3])
+    for qpos in range(max(0, p - d["window"] + 1), p + 1):
+        src = w.ring[0, qpos % d["ring_cap"]] if qpos < L else w.tree_u[0, path[qpos - L]]
+        rows.append(O.bf16_to_f64(src[:d["d_row"]]))
+    R = torch.from_numpy(np.stack(rows))
+    Q = torch.from_numpy(O.bf16_to_f64(w.q[0, 3]))
+    sc = float(np.float32(d["scale"]))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        Q[None], R[None, :, :d["d_k"]], R[None, :, d["v_off"]:d["v_off"] + d["d_v"]], scale=sc)[0]
+    np.testing.assert_allclose(alt["out"], ref.numpy(), atol=1e-12)
