@@ -7,19 +7,32 @@
 // acceptance (Sec. 4.1 chains compressed independently after branching;
 // Sec. 4.2 scratch pad for temporary branch state).
 //
-// One workgroup per (row, node); nodes that close no block exit at once.  The
-// block's token rows (committed ones from the ring, path ones from tree_u) are
-// resolved once into an LDS pointer table; gate logits and the weighted sum
-// then stream the rows with 16-byte loads.
+// One 1024-thread workgroup per (row, node); nodes that close no block exit at
+// once.  A node that closes both a CSA and an HCA block pools suffixes of the
+// same token range (both blocks end at its position), so each token row is
+// read once for the gate logits of both and once for both weighted sums.
+// The rows (committed ones from the ring, path ones from tree_u) are resolved
+// once into an LDS pointer table; gate logits (8 lanes per token, a 128-token
+// block in one pass) and the weighted sums (8 token groups per 16-byte channel
+// chunk) stream them with 16-byte loads, all of a thread's loads in flight
+// together.
 #include "tv_common.h"
 #include "tv_internal.h"
 
 namespace tv {
 
 constexpr int kMaxRatio = 1024;
-constexpr int kMaxDu = 1024;  // raw row width bound (d_row + d_idx), 128 chunks of 16 bytes
+constexpr int kMaxDu = 640;       // raw row width bound (d_row + d_idx): the supported shapes' 640 and 320
+constexpr int kMaxCh = kMaxDu / 8;  // 16-byte chunks of the widest row
+constexpr int kNT = 1024;           // threads per workgroup
+constexpr int kMaxGroups = 16;      // token groups of the weighted sums
 
-__global__ void __launch_bounds__(256) compress_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
+__device__ __forceinline__ float dot8(const float *g, uint4 v) {
+  return g[0] * bf2f_lo(v.x) + g[1] * bf2f_hi(v.x) + g[2] * bf2f_lo(v.y) + g[3] * bf2f_hi(v.y) +
+         g[4] * bf2f_lo(v.z) + g[5] * bf2f_hi(v.z) + g[6] * bf2f_lo(v.w) + g[7] * bf2f_hi(v.w);
+}
+
+__global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
                                                        const uint64_t *__restrict__ anc,
                                                        const int32_t *__restrict__ depth,
                                                        const uint16_t *__restrict__ gate_w,
@@ -27,126 +40,164 @@ __global__ void __launch_bounds__(256) compress_kernel(tv_dims d, CacheView c, c
                                                        int32_t *__restrict__ row_status) {
   __shared__ int32_t path[64];
   __shared__ const uint16_t *tok[kMaxRatio];
-  __shared__ float wgt[kMaxRatio];
-  __shared__ float gate[kMaxDu];
-  __shared__ float part[4][kMaxDu];
-  __shared__ float red[2];
+  __shared__ float wgt[2][kMaxRatio];
+  __shared__ float gate[2][kMaxDu];
+  __shared__ float part[2][kMaxGroups][kMaxDu];
+  __shared__ float red[2][2];
   const int b = blockIdx.x / d.D;
   const int i = blockIdx.x - b * d.D;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int d_u = d.d_row + d.d_idx;
-  if (row_status[b] != TV_ROW_OK) return;
+  const int64_t node = (int64_t)b * d.D + i;
+  // every independent load first, one wait for all of them
+  const int32_t status = row_status[b];
   const int32_t L = c.len[b];
+  const int32_t dep = depth[node];
+  const uint64_t m = anc[node];
+  const int32_t dj = tid < d.D ? depth[(int64_t)b * d.D + tid] : 0;
+  const float g0 = tid < d_u ? bf2f(gate_w[tid]) : 0.f;
+  const float g1 = tid < d_u ? bf2f(gate_w[d_u + tid]) : 0.f;
+  asm volatile("" ::"v"(g0), "v"(g1));  // gate loads issued with the others, not after the checks
+  if (status != TV_ROW_OK) return;
   if (!len_ok(L, d.max_len)) {
     if (i == 0 && tid == 0) row_status[b] = TV_ROW_BAD_LEN;
     return;
   }
-  const int64_t node = (int64_t)b * d.D + i;
-  const int32_t dep = depth[node];
   const int64_t p = (int64_t)L + dep;
-  const bool close4 = ((p + 1) % d.ratio_csa) == 0;
-  const bool close128 = ((p + 1) % d.ratio_hca) == 0;
-  if (!close4 && !close128) return;
-  const uint64_t m = anc[node];
-  for (int j = tid; j < d.D; j += blockDim.x)
-    if ((m >> j) & 1ull) path[depth[(int64_t)b * d.D + j]] = j;
+  const bool cl[2] = {((p + 1) % d.ratio_csa) == 0, ((p + 1) % d.ratio_hca) == 0};
+  if (!cl[0] && !cl[1]) return;
+  const int rat[2] = {d.ratio_csa, d.ratio_hca};
+  const int keep[2] = {d_u, d.d_row};  // CSA entries keep the indexer key, HCA entries the latent row
+  // Both closed blocks end at p: the tokens are positions p-R+1..p of the
+  // larger one, and ratio ri pools the last rat[ri] of them.
+  const int R = std::max(cl[0] ? rat[0] : 0, cl[1] ? rat[1] : 0);
+  const int first[2] = {R - rat[0], R - rat[1]};
+  if (tid < d.D && ((m >> tid) & 1ull)) path[dj] = tid;
+  if (tid < d_u) {
+    gate[0][tid] = g0;
+    gate[1][tid] = g1;
+  }
+  __syncthreads();
+  const int64_t q0 = p - R + 1;
+  for (int t = tid; t < R; t += kNT) {
+    const int64_t qq = q0 + t;
+    tok[t] = qq < L ? ring_row(c.ring, b, d.ring_cap, d_u, qq) : tree_u + ((int64_t)b * d.D + path[qq - L]) * d_u;
+  }
   __syncthreads();
 
-  const int nch = d_u / 8;  // 16-byte chunks per raw row
+  // Gate logits of every token for every ratio that pools it: 8 lanes per
+  // token, 128 tokens per pass, all loads of a lane issued before their use.
+  const int nch = d_u / 8;
+  for (int t0 = 0; t0 < R; t0 += kNT / 8) {
+    const int t = t0 + (tid >> 3), sub = tid & 7;
+    float acc[2] = {0.f, 0.f};
+    if (t < R) {
+      const uint4 *row = reinterpret_cast<const uint4 *>(tok[t]);
+      constexpr int U = (kMaxCh + 7) / 8;
+      uint4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = sub + 8 * u;
+        v[u] = k < nch ? row[k] : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int ri = 0; ri < 2; ++ri) {
+        if (!cl[ri] || t < first[ri]) continue;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = sub + 8 * u;
+          if (k < nch) acc[ri] += dot8(gate[ri] + 8 * k, v[u]);
+        }
+      }
+    }
+#pragma unroll
+    for (int ri = 0; ri < 2; ++ri) {
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) acc[ri] += __shfl_xor(acc[ri], o, 64);
+      if (t < R && sub == 0 && cl[ri] && t >= first[ri]) wgt[ri][t - first[ri]] = acc[ri];
+    }
+  }
+  __syncthreads();
+  // softmax over each pooled block: wave ri
+  if (wv < 2 && cl[wv]) {
+    const int ri = wv, r = rat[ri];
+    float mx = -INFINITY;
+    for (int t = lane; t < r; t += 64) mx = fmaxf(mx, wgt[ri][t]);
+    mx = wave_max(mx);
+    float s = 0.f;
+    for (int t = lane; t < r; t += 64) s += __expf(wgt[ri][t] - mx);
+    s = wave_sum(s);
+    if (lane == 0) {
+      red[ri][0] = mx;
+      red[ri][1] = s;
+    }
+  }
+  __syncthreads();
+#pragma unroll
   for (int ri = 0; ri < 2; ++ri) {
-    if (ri == 0 && !close4) continue;
-    if (ri == 1 && !close128) continue;
-    const int r = ri == 0 ? d.ratio_csa : d.ratio_hca;
-    const int keep = ri == 0 ? d_u : d.d_row;
-    const int64_t q0 = p - r + 1;
-    for (int t = tid; t < r; t += blockDim.x) {
-      const int64_t qq = q0 + t;
-      tok[t] = qq < L ? ring_row(c.ring, b, d.ring_cap, d_u, qq) : tree_u + ((int64_t)b * d.D + path[qq - L]) * d_u;
-    }
-    for (int ch = tid; ch < d_u; ch += blockDim.x) gate[ch] = bf2f(gate_w[(int64_t)ri * d_u + ch]);
-    __syncthreads();
-    // gate logits: 8 lanes per token, each a strided set of 16-byte chunks
-    // (all loads of a lane issued before their use; rows hold at most 128 chunks)
-    for (int t0 = 0; t0 < r; t0 += 32) {
-      const int t = t0 + (tid >> 3), sub = tid & 7;
-      float acc = 0.f;
-      if (t < r) {
-        const uint4 *row = reinterpret_cast<const uint4 *>(tok[t]);
-        uint4 v[16];
+    if (!cl[ri]) continue;
+    const float mx = red[ri][0], inv = 1.0f / red[ri][1];
+    for (int t = tid; t < rat[ri]; t += kNT) wgt[ri][t] = __expf(wgt[ri][t] - mx) * inv;
+  }
+  __syncthreads();
+
+  // Weighted sums: thread (token group g, chunk k) sums 8 channels over the
+  // tokens g, g + G, ... of the block, each read once and added to every
+  // ratio that pools it; a thread's token loads (at most twelve for the
+  // supported shapes and ratios) are in flight together.
+  const int kc = std::max(cl[0] ? keep[0] / 8 : 0, cl[1] ? keep[1] / 8 : 0);
+  const int G = std::min(kMaxGroups, kNT / kc);
+  {
+    const int g = tid / kc, k = tid - g * kc;
+    float acc[2][8];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int k = sub + 8 * u;
-          v[u] = k < nch ? row[k] : make_uint4(0, 0, 0, 0);
+    for (int ri = 0; ri < 2; ++ri)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[ri][e] = 0.f;
+    if (g < G) {
+      for (int tb = g; tb < R; tb += 12 * G) {
+        uint4 v[12];
+#pragma unroll
+        for (int u = 0; u < 12; ++u) {
+          const int t = tb + G * u;
+          v[u] = t < R ? reinterpret_cast<const uint4 *>(tok[t])[k] : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int k = sub + 8 * u;
-          if (k < nch) {
-            const float *gk = gate + 8 * k;
-            acc += gk[0] * bf2f_lo(v[u].x) + gk[1] * bf2f_hi(v[u].x) + gk[2] * bf2f_lo(v[u].y) +
-                   gk[3] * bf2f_hi(v[u].y) + gk[4] * bf2f_lo(v[u].z) + gk[5] * bf2f_hi(v[u].z) +
-                   gk[6] * bf2f_lo(v[u].w) + gk[7] * bf2f_hi(v[u].w);
+        for (int u = 0; u < 12; ++u) {
+          const int t = tb + G * u;
+#pragma unroll
+          for (int ri = 0; ri < 2; ++ri) {
+            if (!(cl[ri] && t < R && t >= first[ri] && k < keep[ri] / 8)) continue;
+            const float w = wgt[ri][t - first[ri]];
+            acc[ri][0] += w * bf2f_lo(v[u].x);
+            acc[ri][1] += w * bf2f_hi(v[u].x);
+            acc[ri][2] += w * bf2f_lo(v[u].y);
+            acc[ri][3] += w * bf2f_hi(v[u].y);
+            acc[ri][4] += w * bf2f_lo(v[u].z);
+            acc[ri][5] += w * bf2f_hi(v[u].z);
+            acc[ri][6] += w * bf2f_lo(v[u].w);
+            acc[ri][7] += w * bf2f_hi(v[u].w);
           }
         }
       }
 #pragma unroll
-      for (int o = 1; o < 8; o <<= 1) acc += __shfl_xor(acc, o, 64);
-      if (t < r && sub == 0) wgt[t] = acc;
-    }
-    __syncthreads();
-    if (wv == 0) {
-      float mx = -INFINITY;
-      for (int t = lane; t < r; t += 64) mx = fmaxf(mx, wgt[t]);
-      mx = wave_max(mx);
-      float s = 0.f;
-      for (int t = lane; t < r; t += 64) s += __expf(wgt[t] - mx);
-      s = wave_sum(s);
-      if (lane == 0) {
-        red[0] = mx;
-        red[1] = s;
-      }
-    }
-    __syncthreads();
-    const float mx = red[0], inv = 1.0f / red[1];
-    for (int t = tid; t < r; t += blockDim.x) wgt[t] = __expf(wgt[t] - mx) * inv;
-    __syncthreads();
-    // weighted sum: thread (token group wv of 4, chunk k) sums 8 channels over
-    // tokens wv, wv+4, ...; loads are issued eight tokens at a time
-    const int kch = keep / 8;
-    for (int k0 = 0; k0 < kch; k0 += 64) {
-      const int k = k0 + lane;
-      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      if (k < kch) {
-        for (int tb = wv; tb < r; tb += 32) {
-          uint4 v[8];
+      for (int ri = 0; ri < 2; ++ri)
+        if (cl[ri] && k < keep[ri] / 8)
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int t = tb + 4 * u;
-            v[u] = t < r ? reinterpret_cast<const uint4 *>(tok[t])[k] : make_uint4(0, 0, 0, 0);
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int t = tb + 4 * u;
-            const float w = t < r ? wgt[t] : 0.f;
-            acc[0] += w * bf2f_lo(v[u].x);
-            acc[1] += w * bf2f_hi(v[u].x);
-            acc[2] += w * bf2f_lo(v[u].y);
-            acc[3] += w * bf2f_hi(v[u].y);
-            acc[4] += w * bf2f_lo(v[u].z);
-            acc[5] += w * bf2f_hi(v[u].z);
-            acc[6] += w * bf2f_lo(v[u].w);
-            acc[7] += w * bf2f_hi(v[u].w);
-          }
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) part[wv][8 * k + e] = acc[e];
-      }
+          for (int e = 0; e < 8; ++e) part[ri][g][8 * k + e] = acc[ri][e];
     }
-    __syncthreads();
+  }
+  __syncthreads();
+#pragma unroll
+  for (int ri = 0; ri < 2; ++ri) {
+    if (!cl[ri]) continue;
     uint16_t *dst = ri == 0 ? scr_c4 + node * d_u : scr_c128 + node * d.d_row;
-    for (int ch = tid; ch < keep; ch += blockDim.x)
-      dst[ch] = f2bf((part[0][ch] + part[1][ch]) + (part[2][ch] + part[3][ch]));
-    __syncthreads();
+    for (int ch = tid; ch < keep[ri]; ch += kNT) {
+      float sum = 0.f;
+#pragma unroll
+      for (int gg = 0; gg < G; ++gg) sum += part[ri][gg][ch];  // group order
+      dst[ch] = f2bf(sum);
+    }
   }
 }
 
@@ -155,7 +206,7 @@ hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t 
                            int32_t *row_status, hipStream_t s) {
   if (d.d_row + d.d_idx > kMaxDu) return hipErrorInvalidValue;
   dim3 grid(d.B * d.D);
-  compress_kernel<<<grid, 256, 0, s>>>(d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status);
+  compress_kernel<<<grid, kNT, 0, s>>>(d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status);
   return hipGetLastError();
 }
 
