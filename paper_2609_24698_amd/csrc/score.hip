@@ -6,8 +6,8 @@
 // so the product runs on MFMA (v_mfma_f32_32x32x16_bf16, float32 accumulate);
 // the head reduction runs in a fixed order so scores are bitwise repeatable.
 //
-// Persistent grid: workgroups stride over the (row, 128-entry chunk) list of
-// all valid rows, so ragged lengths cost no idle workgroups.
+// General path: a persistent grid strides over the (row, 128-entry chunk)
+// list of all valid rows, so ragged lengths cost no idle workgroups.
 #include <algorithm>
 
 #include "tv_common.h"
@@ -152,102 +152,87 @@ __global__ void __launch_bounds__(256) score_kernel(tv_dims d, CacheView c, cons
 // layout a lane holds, for entry column l32, heads 4 hi + 0..3 of nodes
 // 4 tile + 0..3.  The weighted ReLU sum over a node's 8 heads is four
 // in-lane terms plus the other half-wave's four (one shuffle), in fixed order.
-// Each workgroup-iteration scores 256 entries (64 per wavefront).
-constexpr int kFastChunk = 256;
+// One workgroup per (row, 256-entry chunk) of the longest possible row, 64
+// entries per wavefront; the loads a chunk needs (row status, length, pool
+// base, indexer weights, then queries and keys) are issued as early as their
+// addresses are known, so a chunk costs two memory round trips.
+constexpr int kFastChunk = 256;  // 4 wavefronts x 64 entries
 
 __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, const uint16_t *__restrict__ q_idx,
                                                        const uint16_t *__restrict__ w_idx,
                                                        const int32_t *__restrict__ row_status,
-                                                       float *__restrict__ scores, int score_stride) {
-  __shared__ int chunk_pref[kMaxB + 1];
-  __shared__ int scan_tmp[4];
+                                                       float *__restrict__ scores, int score_stride,
+                                                       int chunks_per_row) {
   __shared__ float wsh[64];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
-
-  const int per = (d.B + 255) / 256;
-  int mine = 0;
-  for (int k = 0; k < per; ++k) {
-    const int b = tid * per + k;
-    if (b < d.B) {
-      const int32_t L = c.len[b];
-      const bool ok = row_status[b] == TV_ROW_OK && len_ok(L, d.max_len);
-      mine += ok ? (L / d.ratio_csa + kFastChunk - 1) / kFastChunk : 0;
-    }
-  }
-  int excl;
-  const int total = block_excl_scan(mine, scan_tmp, &excl);
-  for (int k = 0, run = excl; k < per; ++k) {
-    const int b = tid * per + k;
-    if (b < d.B) {
-      chunk_pref[b] = run;
-      const int32_t L = c.len[b];
-      const bool ok = row_status[b] == TV_ROW_OK && len_ok(L, d.max_len);
-      run += ok ? (L / d.ratio_csa + kFastChunk - 1) / kFastChunk : 0;
-    }
-  }
-  if (tid == 0) chunk_pref[d.B] = total;
-  __syncthreads();
-
+  const int b = blockIdx.x / chunks_per_row;
+  const int ch = blockIdx.x - b * chunks_per_row;
   const int M = d.D * 8;
-  for (int cid = blockIdx.x; cid < total; cid += gridDim.x) {
-    int lo = 0, hi2 = d.B - 1;
-    while (lo < hi2) {
-      const int mid = (lo + hi2 + 1) >> 1;
-      if (chunk_pref[mid] <= cid) lo = mid; else hi2 = mid - 1;
+  const int32_t status = row_status[b];
+  const int32_t L = c.len[b];
+  const int64_t c4b = c.c4_base[b];
+  const float wv_ = tid < M ? bf2f(w_idx[(int64_t)b * M + tid]) : 0.f;
+  if (status != TV_ROW_OK || !len_ok(L, d.max_len)) return;
+  const int n4 = L / d.ratio_csa;
+  const int e0 = ch * kFastChunk + wv * 64;
+  if (ch * kFastChunk >= n4) return;
+  // A: query rows 32 t + l32, channels 16 ks + 8 hi (issued with the keys)
+  bf16x8 qa[2][4];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int r = t * 32 + l32;
+    const uint4 *src = reinterpret_cast<const uint4 *>(q_idx + ((int64_t)b * M + (r < M ? r : 0)) * 64);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = r < M ? src[ks * 2 + hi] : make_uint4(0, 0, 0, 0);
+      qa[t][ks] = __builtin_bit_cast(bf16x8, v);
     }
-    const int b = lo;
-    const int n4 = c.len[b] / d.ratio_csa;
-    const int e0 = (cid - chunk_pref[b]) * kFastChunk + wv * 64;
-    if (tid < 64) wsh[tid] = tid < M ? bf2f(w_idx[(int64_t)b * M + tid]) : 0.f;
-    __syncthreads();
-    // A: query rows 32 t + l32, channels 16 ks + 8 hi
-    bf16x8 qa[2][4];
+  }
+  bf16x8 kb[2][4];
+#pragma unroll
+  for (int cc = 0; cc < 2; ++cc) {
+    const int e = e0 + cc * 32 + l32;
+    const bool live = e < n4;
+    const uint4 *ksrc = reinterpret_cast<const uint4 *>(c.c4_idx + (c4b + (live ? e : 0)) * 64);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      kb[cc][ks] = __builtin_bit_cast(bf16x8, live ? ksrc[ks * 2 + hi] : make_uint4(0, 0, 0, 0));
+  }
+  if (tid < 64) wsh[tid] = wv_;
+  __syncthreads();
+#pragma unroll
+  for (int cc = 0; cc < 2; ++cc) {
+    const int e = e0 + cc * 32 + l32;
+    const bool live = e < n4;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int r = t * 32 + l32;
-      const uint4 *src = reinterpret_cast<const uint4 *>(q_idx + ((int64_t)b * M + (r < M ? r : 0)) * 64);
+      f32x16 acc = f32x16{};
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const uint4 v = r < M ? src[ks * 2 + hi] : make_uint4(0, 0, 0, 0);
-        qa[t][ks] = __builtin_bit_cast(bf16x8, v);
+      for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[t][ks], kb[cc][ks], acc, 0, 0, 0);
+      // head reduction of node 4t + J: rows 8J + 4hi + r of the tile, the
+      // two halves combined in a fixed order
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        const int nd = 4 * t + J;
+        float sp = 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sp += wsh[8 * nd + 4 * hi + r] * fmaxf(acc[4 * J + r], 0.f);
+        const float other = __shfl_xor(sp, 32, 64);
+        const float sfull = hi == 0 ? sp + other : other + sp;
+        if (hi == (J & 1) && nd < d.D && live) scores[((int64_t)b * d.D + nd) * score_stride + e] = sfull;
       }
     }
-#pragma unroll
-    for (int cc = 0; cc < 2; ++cc) {
-      const int e = e0 + cc * 32 + l32;
-      const bool live = e < n4;
-      const uint4 *ksrc = reinterpret_cast<const uint4 *>(c.c4_idx + (c.c4_base[b] + (live ? e : 0)) * 64);
-      bf16x8 kb[4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kb[ks] = __builtin_bit_cast(bf16x8, live ? ksrc[ks * 2 + hi] : make_uint4(0, 0, 0, 0));
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        f32x16 acc = f32x16{};
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[t][ks], kb[ks], acc, 0, 0, 0);
-#pragma unroll
-        for (int J = 0; J < 4; ++J) {
-          const int nd = 4 * t + J;
-          float sp = 0.f;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sp += wsh[8 * nd + 4 * hi + r] * fmaxf(acc[4 * J + r], 0.f);
-          const float other = __shfl_xor(sp, 32, 64);
-          const float sfull = hi == 0 ? sp + other : other + sp;
-          if (hi == (J & 1) && nd < d.D && live) scores[((int64_t)b * d.D + nd) * score_stride + e] = sfull;
-        }
-      }
-    }
-    __syncthreads();
   }
 }
 
 hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
                         const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s) {
   if (d.H_idx == 8 && d.D <= 8) {
-    const int64_t upper = (int64_t)d.B * ((d.max_len / d.ratio_csa + kFastChunk - 1) / kFastChunk);
-    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(upper, 2048));
-    score_kernel_h8<<<grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride);
+    const int chunks = std::max(1, (d.max_len / d.ratio_csa + kFastChunk - 1) / kFastChunk);
+    const int64_t grid = (int64_t)d.B * chunks;
+    if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+    score_kernel_h8<<<(unsigned)grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride, chunks);
     return hipGetLastError();
   }
   const int64_t upper = (int64_t)d.B * ((d.max_len / d.ratio_csa + kScoreChunk - 1) / kScoreChunk);
