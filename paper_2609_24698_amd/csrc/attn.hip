@@ -51,13 +51,22 @@ struct AttnShape {
   static_assert((DK / 16) % NP == 0, "key width must split over the wavefronts");
   static_assert(DVW % 32 == 0, "value width must split into 32-wide tiles");
   static_assert(CPR % 8 == 0, "rows must be whole 128-byte groups");
-  // XOR swizzle of the low three bits of a row's 16-byte chunk index; with
-  // 72-chunk rows it spreads one chunk column of 16 consecutive rows over all
-  // 16 four-bank groups of the 64 LDS banks.
-  __device__ static __forceinline__ int swz(int r) { return CPR % 16 == 8 ? ((r >> 1) & 7) : (r & 7); }
+  // Own-copy layout: when each wave's value channels are exactly one
+  // 128-byte column group of the rows (and one group of rope channels is
+  // left), the tile is stored group-major (group g of all 32 rows, then group
+  // g+1, ...).  Wave w then copies column group w of the next tile itself, as
+  // soon as its own P V reads of the buffer are done, with no barrier.
+  static constexpr bool OWN = VOFF == 0 && DVW == 64 && CPR == 8 * (NW + 1);
+  static constexpr int GROUP_BYTES = kKT * 128;     // one column group of the tile (OWN)
+  static constexpr int KSTRIDE = OWN ? GROUP_BYTES : 128;  // bytes between logit k-steps 4m and 4m+4
+  // XOR swizzle of the low three bits of a row's 16-byte chunk index: one
+  // chunk column of 16 consecutive rows lands on all 16 four-bank groups of
+  // the 64 LDS banks (the row stride is 8 chunks mod 16 in both layouts).
+  __device__ static constexpr int swz(int r) { return (OWN || CPR % 16 == 8) ? ((r >> 1) & 7) : (r & 7); }
   // byte offset in a tile of element `col` of row `r`
-  __device__ static __forceinline__ int off(int r, int col) {
+  __device__ static constexpr int off(int r, int col) {
     const int c = col >> 3;
+    if (OWN) return (c >> 3) * GROUP_BYTES + r * 128 + ((c & 7) ^ swz(r)) * 16 + (col & 7) * 2;
     return (r * CPR + (c & ~7) + ((c & 7) ^ swz(r))) * 16 + (col & 7) * 2;
   }
 };
@@ -182,15 +191,6 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
     for (int ct = 0; ct < S::CT; ++ct)
       voff[rr][ct] = S::off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
                             VOFF + wv * S::DVW + 16 * (g & 1) + 4 * (jj & 3) + 32 * ct);
-  // Gather map: instruction k of this wave fills physical chunk P = (wv + NW k)*64 + lane,
-  // which holds logical chunk (P % CPR) ^ swz(row) of row P / CPR.
-  int gmap[S::NPW];
-#pragma unroll
-  for (int k = 0; k < S::NPW; ++k) {
-    const int P = (wv + NW * k) * 64 + lane;
-    const int r = P / S::CPR;
-    gmap[k] = r | ((((P - r * S::CPR) ^ S::swz(r)) * 16) << 8);
-  }
   // partial-logit exchange slots: chunk u of lane l sits at u ^ ((l >> 2) & 3)
   const int xsw = (lane >> 2) & 3;
   __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers before the loop
@@ -200,23 +200,51 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   // Source addresses of this wave's copies of the next tile to issue, read
   // from the pointer table one phase ahead of the copies.  Rows past the
   // split's end re-read its last key (finite data, probability forced to 0).
+  //   own-copy layout: instruction k < 4 fills rows 8k..8k+7 of column group
+  //   wv (lane = row-in-8 * 8 + slot); instruction 4 fills rows 4wv..4wv+3 of
+  //   the rope group (lanes 0..31).  Slot s of row r holds logical chunk
+  //   s ^ swz(r) of the group.
+  //   row-major layout: instruction k fills physical chunk P = (wv + NW k)*64
+  //   + lane, which holds logical chunk (P % CPR) ^ swz(row) of row P / CPR.
   const unsigned char *nsrc[S::NPW];
   auto load_srcs = [&](int tile) {
 #pragma unroll
     for (int k = 0; k < S::NPW; ++k) {
-      const int t = std::min(tile * kKT + (gmap[k] & 255), nkeys - 1);
-      nsrc[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + (gmap[k] >> 8);
+      int r, c;
+      if constexpr (S::OWN) {
+        const int s8 = lane & 7;
+        if (k < S::NPW - 1) {
+          r = 8 * k + (lane >> 3);
+          c = 8 * wv + (s8 ^ S::swz(r));
+        } else {
+          r = 4 * wv + ((lane & 31) >> 3);
+          c = 8 * NW + (s8 ^ S::swz(r));
+        }
+      } else {
+        const int P = (wv + NW * k) * 64 + lane;
+        r = P / S::CPR;
+        c = (P - r * S::CPR) ^ S::swz(r);
+      }
+      const int t = std::min(tile * kKT + r, nkeys - 1);
+      nsrc[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + c * 16;
     }
   };
   auto issue_tile = [&](int buf) {
 #pragma unroll
     for (int k = 0; k < S::NPW; ++k) {
-      const int ins = wv + NW * k;
-      if (S::NINS % NW == 0 || ins < S::NINS) dma16(nsrc[k], lds_base + buf * S::TILE_BYTES + ins * 1024);
+      if constexpr (S::OWN) {
+        if (k < S::NPW - 1)
+          dma16(nsrc[k], lds_base + buf * S::TILE_BYTES + wv * S::GROUP_BYTES + k * 1024);
+        else if (lane < 32)
+          dma16(nsrc[k], lds_base + buf * S::TILE_BYTES + NW * S::GROUP_BYTES + wv * 512);
+      } else {
+        const int ins = wv + NW * k;
+        if (S::NINS % NW == 0 || ins < S::NINS) dma16(nsrc[k], lds_base + buf * S::TILE_BYTES + ins * 1024);
+      }
     }
   };
   // vmcnt bound that leaves this wave's copies of the newest tile in flight
-  const bool full_share = S::NINS % NW == 0 || wv + NW * (S::NPW - 1) < S::NINS;
+  const bool full_share = S::OWN || S::NINS % NW == 0 || wv + NW * (S::NPW - 1) < S::NINS;
 
   f32x16 acc_o[HT][S::CT];
   float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
@@ -243,7 +271,7 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
     const unsigned char *kt = sK[it % NBUF];
     bf16x8 a[S::KSP];
 #pragma unroll
-    for (int m = 0; m < S::KSP; ++m) a[m] = *reinterpret_cast<const bf16x8 *>(kt + aoff + 128 * m);
+    for (int m = 0; m < S::KSP; ++m) a[m] = *reinterpret_cast<const bf16x8 *>(kt + aoff + S::KSTRIDE * m);
     f32x16 sacc = f32x16{};
 #pragma unroll
     for (int m = 0; m < S::KSP; ++m) sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m], qf[m], sacc, 0, 0, 0);
@@ -333,7 +361,8 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   // every wave before this phase), then, after the probabilities, the wait
   // for tile t+1.
   auto issue_next = [&](int t) {
-    if (t + 2 < ntiles) issue_tile((t + 2) % NBUF);
+    if constexpr (!S::OWN)
+      if (t + 2 < ntiles) issue_tile((t + 2) % NBUF);
   };
   auto wait_next = [&](int t) {
     if (t + 2 < ntiles) {
@@ -365,7 +394,12 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       issue_tile(1);
     }
     if (ntiles > 2) load_srcs(2);
-    vm_wait<0>();
+    if constexpr (S::OWN) {  // tile 2 goes into the third buffer at once
+      if (ntiles > 2) issue_tile(2);
+      wait_next(0);
+    } else {
+      vm_wait<0>();
+    }
     __syncthreads();
     qk_tile(0);
     lds_barrier();
@@ -382,12 +416,15 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       int anyf = 0;  // overflow flags of the probabilities of tile it
 #pragma unroll
       for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
-      if (it + 3 < ntiles) load_srcs(it + 3);  // copied in the next phase
+      if (it + 3 < ntiles) load_srcs(it + 3);  // copied in this phase (own copy) or the next
       if (more) qk_tile(it + 1);
       pv_tile(it);
       if (anyf) {  // probabilities of tile it overflowed the reference
         restart = attempt < kMaxRestarts;
         if (restart) break;
+      }
+      if constexpr (S::OWN) {  // this wave's reads of tile it are done: its groups of tile it+3 go there
+        if (it + 3 < ntiles) issue_tile(it % NBUF);
       }
       if (!more) break;
       lds_barrier();
