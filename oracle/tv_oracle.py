@@ -22,6 +22,12 @@ What it computes, with the paper passage each step follows:
 * ``commit_accepted_path``: refresh of token history, window KV and the
   compressed states along the accepted path only (Sec. 3.2 and Sec. 4.2,
   accepted-path refresh; rejected branches leave no trace).
+* ``select_accepted_path``: accepted-path selection after verification
+  (Sec. 4.1: target verify ends by selecting the accepted path; Sec. 3.1: the
+  result is one path through the tree, not a prefix length; Sec. 4.4: selection
+  precedes the state refresh).  Greedy verification in the EAGLE/MTP setting of
+  Sec. 2.1: a draft token is accepted when it equals the target model's
+  highest-scoring next token at its parent.
 
 The paper cites DeepSeek-V4 for the CSA/HCA arithmetic without restating it.
 The reading taken here (kept identical on the GPU side):
@@ -366,6 +372,60 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
         al[b] = len(path)
     return dict(ring=ring, c4=c4, c4_idx=c4_idx, c128=c128, lens=lens, status=status,
                 accept_nodes=an, accept_len=al)
+
+
+# --------------------------------------------------------------------------
+# accepted-path selection
+# --------------------------------------------------------------------------
+def target_argmax(logits_bits) -> np.ndarray:
+    """Index of the largest logit along the last axis; the first one on ties.
+
+    Logits are bfloat16 bit patterns widened exactly.  A NaN counts as larger
+    than every number (the first NaN wins), and -0 equals +0.
+    """
+    x = bf16_to_f64(logits_bits)
+    return np.argmax(x, axis=-1).astype(np.int32)
+
+
+def select_accepted_path(parents, draft_tokens, target_logits, row_status):
+    """Greedy accepted-path selection over each row's draft tree.
+
+    The target token of node i is the argmax of its logits (the target
+    model's next token after node i's prefix).  A non-root node matches when
+    its draft token equals its parent's target token, and a node is accepted
+    when every non-root node on its root path matches (the root is the token
+    the previous round already produced).  The accepted path ends at the
+    deepest accepted node; among equally deep ones, the smallest index
+    (siblings drafted with equal tokens are the only way to get a tie).
+    Rows whose status is not OK are skipped: their outputs are -1.
+
+    Returns (target_tokens [B][D], accepted_last [B], next_token [B]), where
+    next_token is the target token of the accepted node (the token the next
+    round starts from).
+    """
+    parents = np.asarray(parents, dtype=np.int64)
+    draft = np.asarray(draft_tokens, dtype=np.int64)
+    B, D = parents.shape
+    tgt_all = target_argmax(target_logits)
+    tgt = np.full((B, D), -1, dtype=np.int32)
+    acc = np.full(B, -1, dtype=np.int32)
+    nxt = np.full(B, -1, dtype=np.int32)
+    for b in range(B):
+        if row_status[b] != ROW_OK:
+            continue
+        tgt[b] = tgt_all[b]
+        best, best_depth = 0, 0
+        for i in range(1, D):
+            ok, j, dep = True, i, 0
+            while j != 0:  # walk the root path of i
+                ok = ok and draft[b, j] == tgt[b, parents[b, j]]
+                j = int(parents[b, j])
+                dep += 1
+            if ok and dep > best_depth:
+                best, best_depth = i, dep
+        acc[b] = best
+        nxt[b] = tgt[b, best]
+    return tgt, acc, nxt
 
 
 def run_round(wl, nodes=None):

@@ -6,6 +6,9 @@ method's arithmetic (no masks, compression, scoring or attention).
 """
 from .inputs import (  # noqa: F401
     CONFIGS,
+    VOCAB,
+    Selection,
+    make_selection,
     Workload,
     make_workload,
     config_dims,

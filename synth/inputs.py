@@ -252,3 +252,70 @@ def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
         c4_base=c4_base, c4_cap=c4_cap, c128_base=c128_base, c128_cap=c128_cap,
         tree_u=tree_u, q=q, q_idx=q_idx, w_idx=w_idx, gate_w=gate_w,
     )
+
+
+# DeepSeek-V3's vocabulary size; the paper does not state DeepSeek-V4's, so the
+# selection workloads take its predecessor's.
+VOCAB = 129280
+
+
+@dataclasses.dataclass
+class Selection:
+    vocab: int
+    draft_tokens: np.ndarray    # int32 [B][D] token drafted at each node (the root's is unused)
+    target_logits: np.ndarray   # uint16 [B][D][vocab] bfloat16 next-token logits of the target at each node
+    planted_last: np.ndarray    # int32 [B] node whose root path the logits were built to accept
+
+
+def make_selection(wl: Workload, vocab: int = VOCAB, seed: Optional[int] = None, *, dup_rows: int = 0,
+                   peak: float = 16.0, noise_std: float = 1.0) -> Selection:
+    """Draft tokens and target logits over the trees of ``wl``.
+
+    Siblings draft distinct tokens (a top-k drafter proposes different tokens
+    at one node), except in the first ``dup_rows`` rows, where the second child
+    of the first node with two children repeats its elder sibling's token.
+    Logits are N(0, noise_std) bfloat16 noise; along the root path of
+    ``wl.accepted_last`` the logits of each node peak (value ``peak``) at the
+    token drafted by the next node of that path, and at the path's last node
+    at a token none of its children drafted, so greedy selection accepts that
+    path.  The draw uses its own generator, so the workload's bytes do not
+    depend on it.
+    """
+    B, D = wl.parents.shape
+    if seed is None:
+        seed = wl.seed + 7919
+    rng = np.random.Generator(np.random.PCG64(seed))
+    draft = rng.integers(0, vocab, size=(B, D)).astype(np.int32)
+    extra = rng.integers(0, vocab, size=(B, D, 8))  # redraws for sibling collisions and the final peak
+    logits = _normal_bf16(rng, (B, D, vocab), std=noise_std)
+    peak_bits = int(_f32_to_bf16_bits(np.array([peak], dtype=np.float32))[0])
+    planted = np.asarray(wl.accepted_last, dtype=np.int32).copy()
+    for b in range(B):
+        par = wl.parents[b]
+        kids = [[c for c in range(1, D) if par[c] == i] for i in range(D)]
+        for i in range(D):  # distinct sibling tokens
+            seen = set()
+            for c in kids[i]:
+                k = 0
+                while int(draft[b, c]) in seen and vocab > len(kids[i]):
+                    draft[b, c] = extra[b, c, k % 8] if k < 8 else (int(draft[b, c]) + 1) % vocab
+                    k += 1
+                seen.add(int(draft[b, c]))
+        if b < dup_rows:
+            for i in range(D):
+                if len(kids[i]) >= 2:
+                    draft[b, kids[i][1]] = draft[b, kids[i][0]]
+                    break
+        path = [int(planted[b])]
+        while par[path[-1]] >= 0:
+            path.append(int(par[path[-1]]))
+        path.reverse()
+        for t in range(len(path) - 1):
+            logits[b, path[t], draft[b, path[t + 1]]] = peak_bits
+        last = path[-1]
+        taken = {int(draft[b, c]) for c in kids[last]}
+        y = int(extra[b, last, 7])
+        while y in taken and vocab > len(taken):
+            y = (y + 1) % vocab
+        logits[b, last, y] = peak_bits
+    return Selection(vocab=vocab, draft_tokens=draft, target_logits=logits, planted_last=planted)
