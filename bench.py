@@ -11,7 +11,10 @@ timed steps with nothing else on the stream; the roofline of the dominant
 kernel (verify attention, HBM bound: algorithmic bytes per launch over its
 mean duration, from HIP event pairs that the library records on the launch
 stream around every kernel during K further timed steps); and the CPU oracle
-timed on a bounded sample of the same workload.
+timed on a bounded sample of the same workload.  Under "next_rows" it adds the
+greedy accepted-path selection over the same trees (target argmax over a
+129,280-token vocabulary at every node, then the path), timed on its own with
+the roofline of its argmax kernel; it is not part of the step.
 """
 from __future__ import annotations
 
@@ -31,7 +34,8 @@ sys.path.insert(0, ROOT)
 METRIC = "verified tree tokens/sec at B=64,D=8,16K ctx; % of MI355X peak HBM GB/s"
 HBM_PEAK_GBS = 8000.0
 DOMINANT = "verify_attn"
-KERNEL_SOURCES = {"verify_attn": ["attn.hip", "node_keys.h", "tv_common.h"]}
+KERNEL_SOURCES = {"verify_attn": ["attn.hip", "node_keys.h", "tv_common.h"],
+                  "target_argmax": ["select.hip", "tv_common.h"]}
 
 WORKLOADS = {
     "C3": "B=64 rows, committed length log-uniform in [1024, 65536] (partially filled 128-token tail), "
@@ -138,6 +142,54 @@ def bench_workload(config: str, steps: int, warmup: int, seed=None):
                                extra_c128=grow // 128 + 4)
 
 
+def pmc_traffic(kernel: str, config: str):
+    """Calibrated HBM bytes per launch from the committed counter summary,
+    or None when the kernel's sources changed since the counters were taken."""
+    pmc_file = os.path.join(ROOT, "profiles", f"{kernel}_{config}_pmc.json")
+    if not os.path.exists(pmc_file):
+        return None
+    with open(pmc_file) as f:
+        pmc = json.load(f)
+    if pmc.get("source_hash") != kernel_source_hash(kernel):
+        return None
+    return pmc.get("hbm_bytes_per_launch")
+
+
+def time_selection(r, wl, K, binding, torch):
+    """Accepted-path selection over the same trees with a vocabulary of
+    synth.VOCAB tokens, timed on its own (it follows verify in a decoding
+    round but is not part of the step): K calls, per-kernel HIP events."""
+    import synth
+
+    sel = synth.make_selection(wl)
+    r.attach_selection(sel)
+    for _ in range(3):
+        r.select()
+    torch.cuda.synchronize()
+    got = r.host("accepted_last")
+    assert np.array_equal(got, sel.planted_last), "selection did not accept the planted paths"
+    stream = torch.cuda.current_stream()
+    binding.tv_profile_enable(2 * K + 4)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(K):
+        r.select()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    kern = binding.tv_profile_read()
+    binding.tv_profile_disable()
+    n, tot = kern["target_argmax"]
+    avg = tot / n
+    a_bytes = wl.B * wl.D * sel.vocab * 2  # every logit read once
+    achieved = a_bytes / (avg / 1e3) / 1e9
+    return {"vocab": sel.vocab, "calls": K, "ms_per_call": round(e0.elapsed_time(e1) / K, 4),
+            "kernels_ms_per_call": {k: round(v[1] / v[0], 4) for k, v in kern.items()},
+            "roofline": {"bound": "hbm", "kernel": "target_argmax", "achieved": round(achieved, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                         "traffic": None, "algorithmic_bytes_per_launch": int(a_bytes),
+                         "avg_launch_ms": round(avg, 5)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -148,6 +200,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check of the first step")
+    ap.add_argument("--no-select", action="store_true",
+                    help="skip the separately timed accepted-path selection (not part of the step)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain elementwise copy of this many MiB five times (HBM counter calibration)")
     args = ap.parse_args()
@@ -245,13 +299,11 @@ def main():
     achieved = a_bytes / (avg_ms / 1e3) / 1e9
     s_bytes = step_bytes(dims, lens0, sel0, depth0, anc0)
 
-    traffic = None
-    pmc_file = os.path.join(ROOT, "profiles", f"{DOMINANT}_{args.config}_pmc.json")
-    if os.path.exists(pmc_file):
-        with open(pmc_file) as f:
-            pmc = json.load(f)
-        if pmc.get("source_hash") == kernel_source_hash(DOMINANT):
-            traffic = pmc.get("hbm_bytes_per_launch")
+    traffic = pmc_traffic(DOMINANT, args.config)
+    select = None
+    if not args.no_select:
+        select = time_selection(r, wl, K, binding, torch)
+        select["roofline"]["traffic"] = pmc_traffic("target_argmax", args.config)
 
     res = {
         "metric": METRIC,
@@ -276,6 +328,10 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(a_bytes), "avg_launch_ms": round(avg_ms, 5)},
     }
+    if select is not None:
+        res["next_rows"] = {"select_accepted_path": select}
+        print(f"[bench] selection: {select['ms_per_call']:.4f} ms per call, argmax "
+              f"{select['roofline']['achieved']:.0f} GB/s", file=sys.stderr, flush=True)
     print(f"[bench] {K} steps in {gpu_ms:.2f} ms GPU ({wall * 1e3:.2f} ms wall); per-kernel ms/step: "
           + ", ".join(f"{k} {v[1] / K:.4f}" for k, v in kern.items()), file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:

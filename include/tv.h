@@ -15,6 +15,8 @@
  *   tv_verify_attention      branch-aware causal verification: every node
  *                            attends to the committed compressed history plus
  *                            its own ancestors only (Sec. 3.1, Sec. 4.1)
+ *   tv_select_accepted_path  greedy accepted-path selection from the target's
+ *                            logits at every node (Sec. 4.1, Sec. 4.4)
  *   tv_commit_accepted_path  accepted-path refresh of token window, CSA and HCA
  *                            state; rejected branches leave no trace (Sec. 3.2,
  *                            Sec. 4.2)
@@ -37,7 +39,8 @@
  *     with 16-byte accesses); a misaligned pointer is TV_ERR_INVALID_ARG.
  *   - The verify workspace must be 256-byte aligned.
  *   - Calls enqueue work on `stream` and return without synchronising the
- *     host.  Issue them in the order mask -> compress -> verify -> commit.
+ *     host.  Issue them in the order mask -> compress -> verify -> select ->
+ *     commit (select is optional when the accepted node is known).
  *   - Floating-point buffers hold bfloat16 bit patterns (uint16_t) unless
  *     stated otherwise; arithmetic is float32 on the device.
  *   - A row is the draft tree of one sequence.  Node 0 is the root; node i has
@@ -181,6 +184,37 @@ tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const ui
                                   const uint16_t *scr_c4, const uint16_t *scr_c128,
                                   const int32_t *accepted_last, int32_t *accept_nodes,
                                   int32_t *accept_len, int32_t *row_status, hipStream_t stream);
+
+/* Bytes of device workspace tv_select_accepted_path needs for these dims and
+ * vocabulary size.  0 on invalid dims or vocab < 1. */
+size_t tv_select_workspace_bytes(const tv_dims *dims, int32_t vocab);
+
+/* Greedy accepted-path selection after verification (Sec. 4.1: target verify
+ * ends by selecting the accepted path; Sec. 3.1: the outcome is one path
+ * through the tree).  The target token of node i is the index of the largest
+ * of its vocab logits (the first one on ties; a NaN counts as the largest, and
+ * -0 equals +0).  A non-root node matches when its draft token equals its
+ * parent's target token; a node is accepted when every non-root node on its
+ * root path matches; the accepted path ends at the deepest accepted node, the
+ * smallest index among equally deep ones.  Called between
+ * tv_verify_attention and tv_commit_accepted_path, whose accepted_last it
+ * produces.
+ *   parents, anc, depth  as read and produced by tv_build_tree_mask (read)
+ *   draft_tokens   int32 [B][D] token drafted at each node; the root's is not read (read)
+ *   target_logits  bfloat16 [B][D][vocab] the target's next-token logits at each node (read)
+ *   target_tokens  int32 [B][D] argmax of each node's logits (written)
+ *   accepted_last  int32 [B] last node of the accepted path (written)
+ *   next_token     int32 [B] target token of accepted_last, the token the next
+ *                  round starts from (written if not NULL)
+ *   row_status     read only: rows whose status is not TV_ROW_OK are skipped
+ *                  and their outputs left as they were
+ *   workspace      device scratch of at least tv_select_workspace_bytes(dims,
+ *                  vocab) bytes, 256-byte aligned, contents on entry ignored */
+tv_status tv_select_accepted_path(const tv_dims *dims, const int32_t *parents, const uint64_t *anc,
+                                  const int32_t *depth, const int32_t *draft_tokens,
+                                  const uint16_t *target_logits, int32_t vocab, int32_t *target_tokens,
+                                  int32_t *accepted_last, int32_t *next_token, const int32_t *row_status,
+                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *tv_status_string(int status);

@@ -19,6 +19,8 @@ from .binding import (  # noqa: F401
     tv_profile_disable,
     tv_profile_enable,
     tv_profile_read,
+    tv_select_accepted_path,
+    tv_select_workspace_bytes,
     tv_verify_attention,
     tv_verify_workspace_bytes,
 )

@@ -21,7 +21,7 @@ ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = range(5)
 
 EXPORTED = (
     "tv_build_tree_mask", "tv_branch_compress", "tv_verify_workspace_bytes", "tv_verify_attention",
-    "tv_commit_accepted_path", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
+    "tv_commit_accepted_path", "tv_select_workspace_bytes", "tv_select_accepted_path", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
 )
 
 
@@ -65,12 +65,15 @@ def lib() -> ctypes.CDLL:
         L.tv_verify_workspace_bytes.restype = sz
         L.tv_verify_attention.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.tv_commit_accepted_path.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tv_select_workspace_bytes.argtypes = [dp, i32]
+        L.tv_select_workspace_bytes.restype = sz
+        L.tv_select_accepted_path.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
         L.tv_status_string.argtypes = [ctypes.c_int]
         L.tv_status_string.restype = ctypes.c_char_p
         L.tv_profile_enable.argtypes = [i32]
         L.tv_profile_read.argtypes = [ctypes.POINTER(TvKernelTime), i32, ctypes.POINTER(i32)]
         for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_commit_accepted_path",
-                     "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
+                     "tv_select_accepted_path", "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -149,6 +152,21 @@ def tv_commit_accepted_path(dims: TvDims, cache: TvCache, tree_u, anc, depth, sc
                                          _ptr(accept_nodes, torch.int32), _ptr(accept_len, torch.int32),
                                          _ptr(row_status, torch.int32), _stream(stream)),
            "tv_commit_accepted_path")
+
+
+def tv_select_workspace_bytes(dims: TvDims, vocab: int) -> int:
+    return int(lib().tv_select_workspace_bytes(ctypes.byref(dims), int(vocab)))
+
+
+def tv_select_accepted_path(dims: TvDims, parents, anc, depth, draft_tokens, target_logits, vocab: int,
+                            target_tokens, accepted_last, next_token, row_status, workspace, stream=None) -> None:
+    _check(lib().tv_select_accepted_path(ctypes.byref(dims), _ptr(parents, torch.int32), _ptr(anc, torch.int64),
+                                         _ptr(depth, torch.int32), _ptr(draft_tokens, torch.int32),
+                                         _ptr(target_logits), int(vocab), _ptr(target_tokens, torch.int32),
+                                         _ptr(accepted_last, torch.int32), _ptr(next_token, torch.int32),
+                                         _ptr(row_status, torch.int32), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)),
+           "tv_select_accepted_path")
 
 
 def tv_profile_enable(capacity: int) -> None:
@@ -239,10 +257,34 @@ class DeviceRound:
                                 t["scr_c128"], t["accepted_last"], t["accept_nodes"], t["accept_len"],
                                 t["row_status"], stream)
 
+    def attach_selection(self, sel, fill: int = -2):
+        """Upload the draft tokens and target logits of ``sel`` (a synth
+        Selection) and allocate the selection outputs and workspace."""
+        t, d = self.t, self.host_dims
+        dev = t["parents"].device
+        self.vocab = int(sel.vocab)
+        t["draft_tokens"] = _dev(sel.draft_tokens.astype(np.int32), dev)
+        t["target_logits"] = _dev(sel.target_logits, dev)
+        t["target_tokens"] = torch.full((d["B"], d["D"]), fill, dtype=torch.int32, device=dev)
+        t["next_token"] = torch.full((d["B"],), fill, dtype=torch.int32, device=dev)
+        ws = tv_select_workspace_bytes(self.dims, self.vocab)
+        if ws == 0:
+            raise TvError(TV_ERR_INVALID_ARG, "tv_select_workspace_bytes")
+        t["select_ws"] = torch.empty(ws, dtype=torch.uint8, device=dev)
+
+    def select(self, stream=None, with_next: bool = True):
+        """Greedy selection; writes accepted_last, which commit then reads."""
+        t = self.t
+        tv_select_accepted_path(self.dims, t["parents"], t["anc"], t["depth"], t["draft_tokens"],
+                                t["target_logits"], self.vocab, t["target_tokens"], t["accepted_last"],
+                                t["next_token"] if with_next else None, t["row_status"], t["select_ws"], stream)
+
     def round(self, stream=None):
         self.mask(stream)
         self.compress(stream)
         self.verify(stream)
+        if "target_logits" in self.t:
+            self.select(stream)
         self.commit(stream)
 
     def host(self, name: str) -> np.ndarray:

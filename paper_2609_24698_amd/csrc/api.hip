@@ -257,6 +257,37 @@ tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const ui
   return TV_OK;
 }
 
+size_t tv_select_workspace_bytes(const tv_dims *dims, int32_t vocab) {
+  if (check_dims(dims) != TV_OK || vocab < 1) return 0;
+  return align256(sizeof(uint64_t) * (size_t)dims->B * dims->D * select_chunks(vocab));
+}
+
+tv_status tv_select_accepted_path(const tv_dims *dims, const int32_t *parents, const uint64_t *anc,
+                                  const int32_t *depth, const int32_t *draft_tokens, const uint16_t *target_logits,
+                                  int32_t vocab, int32_t *target_tokens, int32_t *accepted_last,
+                                  int32_t *next_token, const int32_t *row_status, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (vocab < 1) return TV_ERR_INVALID_ARG;
+  if (!parents || !anc || !depth || !draft_tokens || !target_logits || !target_tokens || !accepted_last ||
+      !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!all_a16(parents, anc, depth, draft_tokens, target_logits, target_tokens, accepted_last, row_status) ||
+      (next_token && !a16(next_token)))
+    return TV_ERR_INVALID_ARG;
+  const size_t need = tv_select_workspace_bytes(dims, vocab);
+  if (!workspace || workspace_bytes < need) return TV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TV_ERR_INVALID_ARG;
+  if ((int64_t)dims->B * dims->D * select_chunks(vocab) > 0x7FFFFFFF) return TV_ERR_UNSUPPORTED;
+  if ((st = check_device()) != TV_OK) return st;
+  uint64_t *part = static_cast<uint64_t *>(workspace);
+  TV_LAUNCH("target_argmax", launch_argmax(*dims, target_logits, vocab, part, stream));
+  TV_LAUNCH("select_path", launch_select(*dims, parents, anc, depth, draft_tokens, vocab, part, row_status,
+                                         target_tokens, accepted_last, next_token, stream));
+  return TV_OK;
+}
+
 tv_status tv_profile_enable(int32_t capacity) {
   if (capacity < 1 || capacity > (1 << 20)) return TV_ERR_INVALID_ARG;
   std::lock_guard<std::mutex> lk(g_prof.mu);

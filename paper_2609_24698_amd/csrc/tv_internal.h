@@ -66,6 +66,13 @@ hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tr
                          const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
                          int32_t *row_status, hipStream_t s);
 
+// Accepted-path selection: chunk keys of the target argmax, then the greedy path.
+int select_chunks(int32_t vocab);
+hipError_t launch_argmax(const tv_dims &d, const uint16_t *logits, int32_t vocab, uint64_t *part, hipStream_t s);
+hipError_t launch_select(const tv_dims &d, const int32_t *parents, const uint64_t *anc, const int32_t *depth,
+                         const int32_t *draft, int32_t vocab, const uint64_t *part, const int32_t *row_status,
+                         int32_t *target, int32_t *accepted_last, int32_t *next_token, hipStream_t s);
+
 // Kernel timing hooks (no-ops unless profiling is enabled).
 void prof_before(const char *name, hipStream_t s);
 void prof_after(hipStream_t s);

@@ -307,7 +307,7 @@ def make_selection(wl: Workload, vocab: int = VOCAB, seed: Optional[int] = None,
                     draft[b, kids[i][1]] = draft[b, kids[i][0]]
                     break
         path = [int(planted[b])]
-        while par[path[-1]] >= 0:
+        while par[path[-1]] >= 0 and len(path) <= D:  # bounded: a broken parent array may loop
             path.append(int(par[path[-1]]))
         path.reverse()
         for t in range(len(path) - 1):

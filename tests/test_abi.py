@@ -97,3 +97,37 @@ def test_misaligned_pointers_rejected_without_gpu():
     cache.c4_idx = bad.value
     assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([ok] * 7), None) == \
         binding.TV_ERR_INVALID_ARG
+
+
+def test_select_arguments_checked_without_gpu():
+    lib = binding.lib()
+    d = _dims()
+    ok, bad = ctypes.c_void_p(1 << 20), ctypes.c_void_p((1 << 20) + 8)
+    assert lib.tv_select_workspace_bytes(ctypes.byref(d), 129280) >= 8 * 2 * 5 * 16
+    need = lib.tv_select_workspace_bytes(ctypes.byref(d), 1000)
+    assert need >= 8 * 2 * 5 and need % 256 == 0
+    assert lib.tv_select_workspace_bytes(ctypes.byref(d), 0) == 0
+    assert lib.tv_select_workspace_bytes(ctypes.byref(_dims(B=0)), 1000) == 0
+    args = [ok] * 5 + [1000] + [ok, ok, None, ok, ok, need]
+    assert lib.tv_select_accepted_path(ctypes.byref(_dims(D=0)), *args, None) == binding.TV_ERR_INVALID_ARG
+    bad_vocab = list(args)
+    bad_vocab[5] = 0
+    assert lib.tv_select_accepted_path(ctypes.byref(d), *bad_vocab, None) == binding.TV_ERR_INVALID_ARG
+    for k in (0, 1, 2, 3, 4, 6, 7, 9):  # every required pointer
+        a = list(args)
+        a[k] = None
+        assert lib.tv_select_accepted_path(ctypes.byref(d), *a, None) == binding.TV_ERR_INVALID_ARG, k
+        a[k] = bad
+        assert lib.tv_select_accepted_path(ctypes.byref(d), *a, None) == binding.TV_ERR_INVALID_ARG, k
+    a = list(args)
+    a[8] = bad  # optional next_token, misaligned
+    assert lib.tv_select_accepted_path(ctypes.byref(d), *a, None) == binding.TV_ERR_INVALID_ARG
+    small = list(args)
+    small[11] = need - 1
+    assert lib.tv_select_accepted_path(ctypes.byref(d), *small, None) == binding.TV_ERR_WORKSPACE
+    nows = list(args)
+    nows[10] = None
+    assert lib.tv_select_accepted_path(ctypes.byref(d), *nows, None) == binding.TV_ERR_WORKSPACE
+    odd = list(args)
+    odd[10] = ctypes.c_void_p((1 << 20) + 16)
+    assert lib.tv_select_accepted_path(ctypes.byref(d), *odd, None) == binding.TV_ERR_INVALID_ARG
