@@ -10,7 +10,9 @@
 // Two launches.  The argmax streams the logits once (B*D*vocab bfloat16, the
 // only sizeable traffic): one workgroup per (node, 8192-entry chunk), each
 // thread with all of its 16-byte loads in flight, reduced to one sortable
-// 64-bit key (value, then lowest index) per chunk.  The selection then runs
+// 64-bit key (value, then lowest index) per chunk.  (A grid-stride loop with
+// the next chunk's loads issued early measured slower: more registers, fewer
+// resident workgroups.)  The selection then runs
 // one wavefront per row: lane i folds node i's chunk keys into its target
 // token, a ballot marks the matching nodes, and the ancestor masks of the
 // verify preprocess decide every node's acceptance at once (no walk).
@@ -41,67 +43,96 @@ __device__ __forceinline__ uint64_t pack(uint32_t key, uint32_t idx) {
 
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
-__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t lo = __shfl_xor((uint32_t)v, o, 64), hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
-    v = umax64(v, (uint64_t(hi) << 32) | lo);
-  }
-  return v;
-}
-
+// Two passes over registers.  The first keeps a float maximum (bfloat16 is
+// exact in float32; fmaxf ignores NaN, which is tracked on the side), about
+// three vector operations per logit.  Only the wavefronts holding the
+// workgroup maximum then look for its first index, so the search costs one
+// wavefront.
 // kVec: vocab % 8 == 0, so every node's logits start on a 16-byte boundary.
 template <bool kVec>
 __global__ void __launch_bounds__(kSelNT) argmax_kernel(const uint16_t *__restrict__ logits, int32_t vocab,
                                                         int chunks, uint64_t *__restrict__ part) {
-  __shared__ uint64_t red[kSelNT / 64];
+  constexpr int kWaves = kSelNT / 64;
+  constexpr int kWords = kVec ? 4 * kSelLoads : kSelChunk / kSelNT / 2;  // 32-bit words (logit pairs) per thread
+  constexpr uint32_t kNegInfPair = 0xFF80FF80u;  // out-of-range logits never beat an in-range one
+  __shared__ float red_max[kWaves];
+  __shared__ int red_nan[kWaves];
+  __shared__ int red_idx[kWaves];
   const int64_t node = blockIdx.x / chunks;
   const int ch = blockIdx.x - (int)node * chunks;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const uint16_t *row = logits + node * vocab;
   const int c0 = ch * kSelChunk;
-  uint64_t best = 0;
+  // index of the logit in the low half of word j of this thread
+  auto first_of = [&](int j) {
+    if constexpr (kVec)
+      return c0 + ((j >> 2) * kSelNT + tid) * 8 + 2 * (j & 3);
+    else
+      return c0 + 2 * (j * kSelNT + tid);
+  };
+  uint32_t w[kWords];
   if constexpr (kVec) {
-    uint4 v[kSelLoads];
 #pragma unroll
     for (int u = 0; u < kSelLoads; ++u) {
-      const int e = c0 + (u * kSelNT + tid) * 8;
-      v[u] = e < vocab ? *reinterpret_cast<const uint4 *>(row + e) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < kSelLoads; ++u) {
-      const int e = c0 + (u * kSelNT + tid) * 8;
-      if (e < vocab) {
-        const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          best = umax64(best, pack(logit_key(w[k]), e + 2 * k));
-          best = umax64(best, pack(logit_key(w[k] >> 16), e + 2 * k + 1));
-        }
-      }
+      const int e = first_of(4 * u);
+      const uint4 v = e < vocab ? *reinterpret_cast<const uint4 *>(row + e)
+                                : make_uint4(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
+      w[4 * u] = v.x;
+      w[4 * u + 1] = v.y;
+      w[4 * u + 2] = v.z;
+      w[4 * u + 3] = v.w;
     }
   } else {
-    constexpr int kPer = kSelChunk / kSelNT;
-    uint16_t v[kPer];
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int e = c0 + u * kSelNT + tid;
-      v[u] = e < vocab ? row[e] : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int e = c0 + u * kSelNT + tid;
-      if (e < vocab) best = umax64(best, pack(logit_key(v[u]), e));
+    for (int j = 0; j < kWords; ++j) {
+      const int e = first_of(j);
+      const uint32_t lo = e < vocab ? row[e] : 0xFF80u, hi = e + 1 < vocab ? row[e + 1] : 0xFF80u;
+      w[j] = lo | (hi << 16);
     }
   }
-  best = wave_max64(best);
-  if ((tid & 63) == 0) red[tid >> 6] = best;
+  float m = -INFINITY;
+  bool nan = false;
+#pragma unroll
+  for (int j = 0; j < kWords; ++j) {
+    const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
+    m = fmaxf(m, fmaxf(lo, hi));
+    nan |= (lo != lo) | (hi != hi);
+  }
+  const float wm = wave_max(m);
+  const bool wnan = __any(nan);
+  if (lane == 0) {
+    red_max[wv] = wm;
+    red_nan[wv] = wnan;
+  }
+  __syncthreads();
+  float M = red_max[0];
+  bool any_nan = red_nan[0];
+#pragma unroll
+  for (int k = 1; k < kWaves; ++k) {
+    M = fmaxf(M, red_max[k]);
+    any_nan = any_nan || red_nan[k];
+  }
+  // the first index holding the maximum (a NaN when there is one), wavefronts that hold it only
+  int idx = 0x7FFFFFFF;
+  if (any_nan ? wnan : wm == M) {
+#pragma unroll
+    for (int j = kWords - 1; j >= 0; --j) {  // backwards: the last hit is the first index
+      const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
+      const int e = first_of(j);
+      if (any_nan ? (hi != hi) : (hi == M)) idx = e + 1 < vocab ? e + 1 : idx;
+      if (any_nan ? (lo != lo) : (lo == M)) idx = e < vocab ? e : idx;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) idx = min(idx, __shfl_xor(idx, o, 64));
+  }
+  if (lane == 0) red_idx[wv] = idx;
   __syncthreads();
   if (tid == 0) {
-    uint64_t m = red[0];
+    int best = red_idx[0];
 #pragma unroll
-    for (int w = 1; w < kSelNT / 64; ++w) m = umax64(m, red[w]);
-    part[blockIdx.x] = m;
+    for (int k = 1; k < kWaves; ++k) best = min(best, red_idx[k]);
+    const uint32_t key = any_nan ? 0xFFFFu : logit_key(__float_as_uint(M) >> 16);
+    part[blockIdx.x] = pack(key, (uint32_t)best);
   }
 }
 
