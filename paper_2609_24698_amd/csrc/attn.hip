@@ -495,48 +495,72 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   }
 }
 
-// Merge the partials of nodes whose keys spanned several splits.
+// Merge the partials of nodes whose keys spanned several splits.  One
+// workgroup per (node, group of heads); a thread owns four value channels of
+// one head and streams that head's partials of every split with 16-byte
+// loads, weighting split s by exp2(m_s - m) / l (m the largest running
+// maximum, l the merged sum), summed in split order.
 template <int DV>
 __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *__restrict__ row_status,
                                                       const int32_t *__restrict__ nkeys_tab, int chunk, int splits,
                                                       const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml, uint16_t *__restrict__ out,
                                                       float *__restrict__ lse) {
-  __shared__ float sW[64][64];  // per (split, head) weight exp2(m_s - m*) / l*
-  const int nodeg = blockIdx.x;
+  constexpr int kTPH = DV / 4;      // threads per head
+  constexpr int kHPW = 256 / kTPH;  // heads per workgroup
+  const int hgroups = (d.H + kHPW - 1) / kHPW;
+  const int nodeg = blockIdx.x / hgroups;
+  const int hg = blockIdx.x - nodeg * hgroups;
   const int b = nodeg / d.D;
-  if (row_status[b] != TV_ROW_OK) return;
+  const int tid = threadIdx.x;
+  const int h = hg * kHPW + tid / kTPH, c4 = tid % kTPH;
+  const int32_t status = row_status[b];
   const int n_keys = nkeys_tab[nodeg];
-  if (n_keys <= chunk) return;
+  if (status != TV_ROW_OK || n_keys <= chunk || h >= d.H) return;
   const int used = (n_keys + chunk - 1) / chunk;
   const int64_t node = nodeg;
-  const int tid = threadIdx.x;
-  for (int h0 = 0; h0 < d.H; h0 += 64) {
-    const int h = h0 + tid;
-    if (tid < 64 && h < d.H) {
-      float mx = -INFINITY;
-      for (int s = 0; s < used; ++s) mx = fmaxf(mx, part_ml[((node * splits + s) * d.H + h) * 2]);
-      float l = 0.f;
-      for (int s = 0; s < used; ++s) {
-        const float* ml = part_ml + ((node * splits + s) * d.H + h) * 2;
-        l += exp2f(ml[0] - mx) * ml[1];
-      }
-      for (int s = 0; s < used; ++s) {
-        const float* ml = part_ml + ((node * splits + s) * d.H + h) * 2;
-        if (s < 64) sW[s][tid] = exp2f(ml[0] - mx) / l;
-      }
-      if (lse) lse[node * d.H + h] = (mx + __log2f(l)) * kLn2;
-    }
-    __syncthreads();
-    const int hn = std::min(64, d.H - h0);
-    for (int e = tid; e < hn * DV; e += 256) {
-      const int hh = e / DV, col = e - hh * DV;
-      float v = 0.f;
-      for (int s = 0; s < used; ++s) v += sW[s][hh] * part_o[((node * splits + s) * d.H + h0 + hh) * DV + col];
-      out[(node * d.H + h0 + hh) * DV + col] = f2bf(v);
-    }
-    __syncthreads();
+  const float2 *ml = reinterpret_cast<const float2 *>(part_ml) + node * splits * d.H + h;  // split s at s * H
+  float mx = -INFINITY;
+  for (int s = 0; s < used; ++s) mx = fmaxf(mx, ml[(int64_t)s * d.H].x);
+  float l = 0.f;
+  for (int s = 0; s < used; ++s) {
+    const float2 v = ml[(int64_t)s * d.H];
+    l += exp2f(v.x - mx) * v.y;
   }
+  const float4 *po = reinterpret_cast<const float4 *>(part_o) + (node * splits * d.H + h) * kTPH + c4;
+  const int64_t pstride = (int64_t)d.H * kTPH;  // next split, same head and channels
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  int s = 0;
+  for (; s + 4 <= used; s += 4) {  // four splits' loads in flight together
+    float4 o[4];
+    float w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      o[k] = po[(s + k) * pstride];
+      w[k] = ml[(int64_t)(s + k) * d.H].x;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float wk = exp2f(w[k] - mx) / l;
+      acc.x += wk * o[k].x;
+      acc.y += wk * o[k].y;
+      acc.z += wk * o[k].z;
+      acc.w += wk * o[k].w;
+    }
+  }
+  for (; s < used; ++s) {
+    const float4 o = po[s * pstride];
+    const float wk = exp2f(ml[(int64_t)s * d.H].x - mx) / l;
+    acc.x += wk * o.x;
+    acc.y += wk * o.y;
+    acc.z += wk * o.z;
+    acc.w += wk * o.w;
+  }
+  uint2 packed;
+  packed.x = uint32_t(f2bf(acc.x)) | (uint32_t(f2bf(acc.y)) << 16);
+  packed.y = uint32_t(f2bf(acc.z)) | (uint32_t(f2bf(acc.w)) << 16);
+  *reinterpret_cast<uint2 *>(out + (node * d.H + h) * DV + 4 * c4) = packed;
+  if (c4 == 0 && lse) lse[node * d.H + h] = (mx + __log2f(l)) * kLn2;
 }
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
@@ -566,7 +590,8 @@ hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_s
 hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
   if (plan.splits <= 1) return hipSuccess;
-  dim3 grid(d.B * d.D);
+  const int hpw = 256 / (d.d_v / 4);
+  dim3 grid(d.B * d.D * ((d.H + hpw - 1) / hpw));
   if (d.d_v == 512)
     combine_kernel<512><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
                                              lse);
