@@ -74,7 +74,11 @@ SplitPlan split_plan(const tv_dims &d) {
   const int64_t mk = (int64_t)d.topk + d.max_len / d.ratio_hca + d.D + d.window;
   p.max_keys = (int32_t)mk;
   const int64_t nodes = (int64_t)d.B * d.D;
-  int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (512 + nodes - 1) / nodes));
+  // Splits only until about 128 workgroups exist: every split pays the
+  // prologue (queries, key table, first tiles) and a partial-output round trip
+  // through memory, which measured costlier than idle compute units (a target
+  // of 128 beat 32..2048 on the B=8 and B=32 workloads and the 1M-token row).
+  int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (128 + nodes - 1) / nodes));
   splits = (int)std::min<int64_t>(splits, (mk + 31) / 32);
   splits = (int)std::max<int64_t>(splits, (mk + kAttnMaxChunk - 1) / kAttnMaxChunk);  // pointer table bound
   int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
@@ -125,7 +129,14 @@ struct Prof {
 } g_prof;
 }  // namespace
 
+// Kernels recorded by the round-graph capture running on this thread (-1: none).
+thread_local int t_capture_kernels = -1;
+
 void prof_before(const char *name, hipStream_t s) {
+  if (t_capture_kernels >= 0) {  // inside a graph capture: count, never time
+    ++t_capture_kernels;
+    return;
+  }
   if (!g_prof.on) return;
   if (g_prof.recs.size() >= g_prof.cap) return;
   ProfRec r{name, g_prof.pool[2 * g_prof.recs.size()], g_prof.pool[2 * g_prof.recs.size() + 1]};
@@ -135,7 +146,7 @@ void prof_before(const char *name, hipStream_t s) {
 }
 
 void prof_after(hipStream_t s) {
-  if (!g_prof.on || !g_prof.pending) return;
+  if (t_capture_kernels >= 0 || !g_prof.on || !g_prof.pending) return;
   hipEventRecord(g_prof.recs.back().stop, s);
   g_prof.pending = false;
 }
@@ -286,6 +297,91 @@ tv_status tv_select_accepted_path(const tv_dims *dims, const int32_t *parents, c
   TV_LAUNCH("select_path", launch_select(*dims, parents, anc, depth, draft_tokens, vocab, part, row_status,
                                          target_tokens, accepted_last, next_token, stream));
   return TV_OK;
+}
+
+}  // extern "C"
+
+struct tv_round_graph {
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+  int32_t kernels;
+};
+
+namespace tv {
+
+// The calls of one round, in order, on stream s (argument checks included).
+static tv_status record_round(const tv_dims *d, const tv_round &r, const tv_layer *layers, int n, hipStream_t s) {
+  tv_status st = tv_build_tree_mask(d, r.parents, r.anc, r.depth, r.row_status, s);
+  for (int l = 0; l < n && st == TV_OK; ++l) {
+    const tv_layer &L = layers[l];
+    st = tv_branch_compress(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status, s);
+    if (st != TV_OK) break;
+    st = tv_verify_attention(d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx,
+                             L.out, L.lse, L.sel, r.row_status, L.workspace, L.workspace_bytes, s);
+  }
+  if (st == TV_OK && r.target_logits)
+    st = tv_select_accepted_path(d, r.parents, r.anc, r.depth, r.draft_tokens, r.target_logits, r.vocab,
+                                 r.target_tokens, r.accepted_last, r.next_token, r.row_status, r.select_workspace,
+                                 r.select_workspace_bytes, s);
+  for (int l = 0; l < n && st == TV_OK; ++l) {
+    tv_cache c = layers[l].cache;
+    st = tv_commit_accepted_path(d, &c, layers[l].tree_u, r.anc, r.depth, layers[l].scr_c4, layers[l].scr_c128,
+                                 r.accepted_last, r.accept_nodes, r.accept_len, r.row_status, s);
+  }
+  return st;
+}
+
+}  // namespace tv
+
+extern "C" {
+
+tv_status tv_round_graph_create(const tv_dims *dims, const tv_round *round, const tv_layer *layers,
+                                int32_t n_layers, tv_round_graph **graph) {
+  if (!graph) return TV_ERR_INVALID_ARG;
+  *graph = nullptr;
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!round || !layers || n_layers < 1 || n_layers > 1024) return TV_ERR_INVALID_ARG;
+  if (!round->target_logits && (round->draft_tokens || round->target_tokens)) return TV_ERR_INVALID_ARG;
+  if ((st = check_device()) != TV_OK) return st;
+  hipStream_t cs = nullptr;
+  if (hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) != hipSuccess) return TV_ERR_DEVICE;
+  if (hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+    (void)hipStreamDestroy(cs);
+    return TV_ERR_LAUNCH;
+  }
+  t_capture_kernels = 0;
+  st = record_round(dims, *round, layers, n_layers, cs);
+  const int32_t kernels = t_capture_kernels;
+  t_capture_kernels = -1;
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(cs, &g);
+  (void)hipStreamDestroy(cs);
+  if (st != TV_OK || e != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    return st != TV_OK ? st : TV_ERR_LAUNCH;
+  }
+  hipGraphExec_t x = nullptr;
+  if (hipGraphInstantiate(&x, g, nullptr, nullptr, 0) != hipSuccess) {
+    (void)hipGraphDestroy(g);
+    return TV_ERR_LAUNCH;
+  }
+  *graph = new tv_round_graph{g, x, kernels};
+  return TV_OK;
+}
+
+int32_t tv_round_graph_kernels(const tv_round_graph *graph) { return graph ? graph->kernels : 0; }
+
+tv_status tv_round_graph_launch(tv_round_graph *graph, hipStream_t stream) {
+  if (!graph) return TV_ERR_INVALID_ARG;
+  return hipGraphLaunch(graph->exec, stream) == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+tv_status tv_round_graph_destroy(tv_round_graph *graph) {
+  if (!graph) return TV_ERR_INVALID_ARG;
+  const bool ok = hipGraphExecDestroy(graph->exec) == hipSuccess && hipGraphDestroy(graph->graph) == hipSuccess;
+  delete graph;
+  return ok ? TV_OK : TV_ERR_LAUNCH;
 }
 
 tv_status tv_profile_enable(int32_t capacity) {
