@@ -22,6 +22,15 @@ What it computes, with the paper passage each step follows:
 * ``commit_accepted_path``: refresh of token history, window KV and the
   compressed states along the accepted path only (Sec. 3.2 and Sec. 4.2,
   accepted-path refresh; rejected branches leave no trace).
+* ``write_through`` and ``commit_accepted_path(primary_last=...)``: the
+  refresh schedules of Sec. 4.3.  The CSA entries of one designated chain are
+  written into the persistent pool while compressing (timely C4 refresh);
+  its entries lie past the committed length, so nothing can see them before
+  the commit makes them committed.  The commit then skips the CSA copies of
+  accepted nodes on that chain (a single chain, or an accepted chain that is
+  already the cached one, needs no CSA refresh), and writes every HCA entry
+  of the accepted path in one go once the path is known (delayed, combined
+  C128 writes).
 * ``select_accepted_path``: accepted-path selection after verification
   (Sec. 4.1: target verify ends by selecting the accepted path; Sec. 3.1: the
   result is one path through the tree, not a prefix length; Sec. 4.4: selection
@@ -317,8 +326,39 @@ def verify_attention(wl, anc, depth, scr_c4, scr_c128, row_status, nodes=None):
 # --------------------------------------------------------------------------
 # accepted-path commit
 # --------------------------------------------------------------------------
+def primary_chain(anc_row, primary_last):
+    """Nodes of a row's designated chain: the root path of ``primary_last``,
+    as a bit set; empty when ``primary_last`` is outside [0, D)."""
+    D = len(anc_row)
+    return int(anc_row[primary_last]) if 0 <= primary_last < D else 0
+
+
+def write_through(wl, anc, depth, scr_c4, w4, primary_last, row_status):
+    """CSA pools after the compression step writes the entries closed on each
+    row's designated chain into their pool slots (logical index
+    ``(p+1)/ratio_csa - 1``, past the committed entries), slot capacity
+    permitting.  ``w4`` marks the scratch slots the compression wrote; rows
+    whose status is not OK write nothing.  Returns new (c4, c4_idx)."""
+    d = wl.dims
+    c4, c4_idx = wl.c4.copy(), wl.c4_idx.copy()
+    d_row = d["d_row"]
+    for b in range(d["B"]):
+        if row_status[b] != ROW_OK:
+            continue
+        chain = primary_chain(anc[b], int(primary_last[b]))
+        L = int(wl.lens[b])
+        for j in range(d["D"]):
+            if not (chain >> j) & 1 or not w4[b, j]:
+                continue
+            s = (L + int(depth[b, j]) + 1) // d["ratio_csa"] - 1
+            if s < wl.c4_cap[b]:
+                c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
+                c4_idx[wl.c4_base[b] + s] = scr_c4[b, j, d_row:]
+    return c4, c4_idx
+
+
 def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_status,
-                         accept_nodes=None, accept_len=None):
+                         accept_nodes=None, accept_len=None, primary_last=None, pools=None):
     """Refresh the committed state along the accepted path of every valid row.
 
     The accepted path is the root path of ``accepted_last[b]`` (a = depth + 1
@@ -326,13 +366,17 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
     nodes that closed a block writes its scratch entry to the pool at the
     entry's logical index, and ``len`` becomes L + a.  A row whose new entries
     would not fit its pool capacity gets status CAPACITY and is left intact.
+    With ``primary_last``, CSA entries of accepted nodes on the row's
+    designated chain are not copied (``write_through`` put them in place);
+    ``pools`` = (c4, c4_idx) then gives the pools as the compression left them.
     Returns a dict of new arrays (inputs are not modified).
     """
     d = wl.dims
     B, D = d["B"], d["D"]
     r4, r128, cap = d["ratio_csa"], d["ratio_hca"], d["ring_cap"]
     d_row = d["d_row"]
-    ring, c4, c4_idx, c128 = wl.ring.copy(), wl.c4.copy(), wl.c4_idx.copy(), wl.c128.copy()
+    ring, c128 = wl.ring.copy(), wl.c128.copy()
+    c4, c4_idx = (wl.c4.copy(), wl.c4_idx.copy()) if pools is None else (pools[0].copy(), pools[1].copy())
     lens = wl.lens.copy()
     status = np.array(row_status, dtype=np.int32).copy()
     an = np.full((B, D), -1, dtype=np.int32) if accept_nodes is None else accept_nodes.copy()
@@ -349,11 +393,14 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
             status[b] = ROW_BAD_ACCEPT
             continue
         path = node_path(anc[b], depth[b], last)
-        writes4, writes128 = [], []
+        chain = 0 if primary_last is None else primary_chain(anc[b], int(primary_last[b]))
+        writes4, writes128, skip4 = [], [], set()
         for j in path:
             p = L + int(depth[b, j])
             if (p + 1) % r4 == 0:
                 writes4.append(((p + 1) // r4 - 1, j))
+                if (chain >> j) & 1:
+                    skip4.add(j)
             if (p + 1) % r128 == 0:
                 writes128.append(((p + 1) // r128 - 1, j))
         if any(s >= wl.c4_cap[b] for s, _ in writes4) or any(s >= wl.c128_cap[b] for s, _ in writes128):
@@ -362,6 +409,8 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
         for t, j in enumerate(path):
             ring[b, (L + t) & (cap - 1)] = wl.tree_u[b, j]
         for s, j in writes4:
+            if j in skip4:
+                continue
             c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
             c4_idx[wl.c4_base[b] + s] = scr_c4[b, j, d_row:]
         for s, j in writes128:
