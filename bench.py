@@ -14,7 +14,9 @@ stream around every kernel during K further timed steps); and the CPU oracle
 timed on a bounded sample of the same workload.  Under "next_rows" it adds the
 greedy accepted-path selection over the same trees (target argmax over a
 129,280-token vocabulary at every node, then the path), timed on its own with
-the roofline of its argmax kernel; it is not part of the step.
+the roofline of its argmax kernel, and a round over 61 layers (DeepSeek-V3's
+depth; the paper does not state V4-Flash's) issued call by call against the
+same round replayed as one HIP graph; neither is part of the step.
 """
 from __future__ import annotations
 
@@ -190,6 +192,46 @@ def time_selection(r, wl, K, binding, torch):
                          "avg_launch_ms": round(avg, 5)}}
 
 
+def time_graph(config: str, n_layers: int, K: int, W: int, torch):
+    """One round over n_layers layers sharing a draft tree (mask once;
+    compress and verify per layer; commit per layer), issued call by call
+    from Python and as one captured graph, on the same device state: K rounds
+    each, HIP events on the stream around the K rounds.  Every layer holds
+    its own copy of the workload's buffers."""
+    from paper_2609_24698_amd import DeviceRound, LayeredRound
+
+    wl = bench_workload(config, K + W + 2, 0)  # the pools take both timings' commits
+    lr = LayeredRound([DeviceRound(wl, "cuda:0", poison_outputs=False) for _ in range(n_layers)])
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(W):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(K):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K, (time.perf_counter() - t0) * 1e3 / K
+
+    eager_ms, eager_wall = timed(lr.eager)
+    kernels = lr.capture()
+    graph_ms, graph_wall = timed(lr.replay)
+    lr.release()
+    status = lr.layers[0].host("row_status")
+    assert np.all(status == 0), f"rows left the workload: {np.unique(status)}"
+    res = {"layers": n_layers, "kernels_per_round": kernels, "eager_ms_per_round": round(eager_ms, 4),
+           "graph_ms_per_round": round(graph_ms, 4), "eager_wall_ms": round(eager_wall, 4),
+           "graph_wall_ms": round(graph_wall, 4), "speedup": round(eager_ms / graph_ms, 3),
+           "tokens_per_s_graph": round(wl.B * wl.D / (graph_ms / 1e3), 1)}
+    del lr
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +244,9 @@ def main():
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check of the first step")
     ap.add_argument("--no-select", action="store_true",
                     help="skip the separately timed accepted-path selection (not part of the step)")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the separately timed multi-layer round (eager calls against one graph replay)")
+    ap.add_argument("--graph-layers", type=int, default=61)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain elementwise copy of this many MiB five times (HBM counter calibration)")
     args = ap.parse_args()
@@ -328,10 +373,23 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(a_bytes), "avg_launch_ms": round(avg_ms, 5)},
     }
+    graph = None
+    if not args.no_graph:
+        graph = {"workloads": {}}
+        for cfg in dict.fromkeys([args.config, "C1"]):
+            graph["workloads"][cfg] = time_graph(cfg, args.graph_layers, K, W, torch)
+    if select is not None or graph is not None:
+        res["next_rows"] = {}
     if select is not None:
-        res["next_rows"] = {"select_accepted_path": select}
+        res["next_rows"]["select_accepted_path"] = select
         print(f"[bench] selection: {select['ms_per_call']:.4f} ms per call, argmax "
               f"{select['roofline']['achieved']:.0f} GB/s", file=sys.stderr, flush=True)
+    if graph is not None:
+        res["next_rows"]["graph_round"] = graph
+        for cfg, g in graph["workloads"].items():
+            print(f"[bench] {cfg} round over {g['layers']} layers: eager {g['eager_ms_per_round']:.3f} ms, "
+                  f"graph {g['graph_ms_per_round']:.3f} ms ({g['kernels_per_round']} kernels)", file=sys.stderr,
+                  flush=True)
     print(f"[bench] {K} steps in {gpu_ms:.2f} ms GPU ({wall * 1e3:.2f} ms wall); per-kernel ms/step: "
           + ", ".join(f"{k} {v[1] / K:.4f}" for k, v in kern.items()), file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:

@@ -216,6 +216,62 @@ tv_status tv_select_accepted_path(const tv_dims *dims, const int32_t *parents, c
                                   int32_t *accepted_last, int32_t *next_token, const int32_t *row_status,
                                   void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ---- Captured multi-layer round (Sec. 4.3: graph replay needs stable
+ * shapes; the tree configuration bounds what one graph covers) -------------
+ *
+ * A model verifies the same draft tree in every layer.  One round is the
+ * verify preprocess once, then per layer the branch compression and verify
+ * attention, then (optionally) the greedy path selection, then per layer the
+ * commit.  tv_round_graph_create records that whole sequence, with every
+ * argument check done once, into one HIP graph; tv_round_graph_launch replays
+ * it on any stream.  A graph is bound to its dims (B, D, max_len: the "D
+ * bucket") and to the buffer addresses given at creation; the tree shape,
+ * token contents and lengths are read from device memory at replay, so new
+ * trees need no new graph.  The graph issues no memory sets and allocates
+ * nothing at replay.  Kernel timing is not recorded inside graphs. */
+
+/* The buffers of one layer: its committed state, the inputs and outputs of
+ * tv_branch_compress and tv_verify_attention for it. */
+typedef struct {
+  tv_cache cache;
+  const uint16_t *tree_u, *gate_w, *q, *q_idx, *w_idx;
+  uint16_t *scr_c4, *scr_c128, *out;
+  float *lse;   /* may be NULL */
+  int32_t *sel; /* may be NULL */
+  void *workspace;
+  size_t workspace_bytes;
+} tv_layer;
+
+/* The buffers every layer of a round shares.  row_status is shared: a row
+ * that fails in any call is skipped by every later call of the round (the
+ * layers committed before the failure keep their commit).  When
+ * target_logits is not NULL the selection runs after the last verify and
+ * writes accepted_last, which every commit then reads; otherwise
+ * accepted_last is an input. */
+typedef struct {
+  const int32_t *parents;
+  uint64_t *anc;
+  int32_t *depth, *row_status, *accepted_last, *accept_nodes, *accept_len;
+  const int32_t *draft_tokens;     /* selection inputs (may be NULL together) */
+  const uint16_t *target_logits;
+  int32_t vocab;
+  int32_t *target_tokens, *next_token;
+  void *select_workspace;
+  size_t select_workspace_bytes;
+} tv_round;
+
+typedef struct tv_round_graph tv_round_graph;
+
+/* Records one round over n_layers layers (1..1024) into a graph.  Returns
+ * the first failing check of any call (nothing is kept then).  The graph is
+ * owned by the caller until tv_round_graph_destroy. */
+tv_status tv_round_graph_create(const tv_dims *dims, const tv_round *round, const tv_layer *layers,
+                                int32_t n_layers, tv_round_graph **graph);
+/* Kernel launches recorded in the graph. */
+int32_t tv_round_graph_kernels(const tv_round_graph *graph);
+tv_status tv_round_graph_launch(tv_round_graph *graph, hipStream_t stream);
+tv_status tv_round_graph_destroy(tv_round_graph *graph);
+
 /* Human-readable name of a status code (static string). */
 const char *tv_status_string(int status);
 

@@ -6,6 +6,7 @@ The compute path is the gfx950 HIP library ``lib/libtv.so`` (C ABI in
 from .binding import (  # noqa: F401
     EXPORTED,
     DeviceRound,
+    LayeredRound,
     TvCache,
     TvDims,
     TvError,

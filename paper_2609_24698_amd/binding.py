@@ -21,7 +21,8 @@ ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = range(5)
 
 EXPORTED = (
     "tv_build_tree_mask", "tv_branch_compress", "tv_verify_workspace_bytes", "tv_verify_attention",
-    "tv_commit_accepted_path", "tv_select_workspace_bytes", "tv_select_accepted_path", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
+    "tv_commit_accepted_path", "tv_select_workspace_bytes", "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_kernels",
+    "tv_round_graph_launch", "tv_round_graph_destroy", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
 )
 
 
@@ -40,6 +41,19 @@ class TvDims(ctypes.Structure):
 class TvCache(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "ring", "c4", "c4_idx", "c128", "c4_base", "c4_cap", "c128_base", "c128_cap", "len")]
+
+
+class TvLayer(ctypes.Structure):
+    _fields_ = [("cache", TvCache)] + [(n, ctypes.c_void_p) for n in (
+        "tree_u", "gate_w", "q", "q_idx", "w_idx", "scr_c4", "scr_c128", "out", "lse", "sel", "workspace")] + [
+        ("workspace_bytes", ctypes.c_size_t)]
+
+
+class TvRound(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "parents", "anc", "depth", "row_status", "accepted_last", "accept_nodes", "accept_len", "draft_tokens",
+        "target_logits")] + [("vocab", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in (
+            "target_tokens", "next_token", "select_workspace")] + [("select_workspace_bytes", ctypes.c_size_t)]
 
 
 class TvKernelTime(ctypes.Structure):
@@ -68,12 +82,19 @@ def lib() -> ctypes.CDLL:
         L.tv_select_workspace_bytes.argtypes = [dp, i32]
         L.tv_select_workspace_bytes.restype = sz
         L.tv_select_accepted_path.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.tv_round_graph_create.argtypes = [dp, ctypes.POINTER(TvRound), ctypes.POINTER(TvLayer), i32,
+                                            ctypes.POINTER(vp)]
+        L.tv_round_graph_kernels.argtypes = [vp]
+        L.tv_round_graph_kernels.restype = i32
+        L.tv_round_graph_launch.argtypes = [vp, vp]
+        L.tv_round_graph_destroy.argtypes = [vp]
         L.tv_status_string.argtypes = [ctypes.c_int]
         L.tv_status_string.restype = ctypes.c_char_p
         L.tv_profile_enable.argtypes = [i32]
         L.tv_profile_read.argtypes = [ctypes.POINTER(TvKernelTime), i32, ctypes.POINTER(i32)]
         for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_commit_accepted_path",
-                     "tv_select_accepted_path", "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
+                     "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_launch",
+                     "tv_round_graph_destroy", "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -294,3 +315,91 @@ class DeviceRound:
         if name == "anc":
             return x.view(np.uint64)
         return x
+
+
+# ---------------------------------------------------------------------------
+# A round over several layers: shared tree buffers, per-layer state.
+# ---------------------------------------------------------------------------
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+class LayeredRound:
+    """One verify round over several layers that share a draft tree.
+
+    ``layers`` are DeviceRound objects (one per layer, each with its own
+    cache, tokens, queries, outputs and workspace); the tree buffers (parents,
+    masks, depths, row status, accepted path) and, when layer 0 has a
+    selection attached, the selection buffers are layer 0's.  ``eager()``
+    issues the calls one by one; ``capture()`` records the same sequence into
+    a HIP graph that ``replay()`` launches.
+    """
+
+    def __init__(self, layers):
+        self.layers = list(layers)
+        self.dims = self.layers[0].dims
+        self.graph = None
+
+    def _shared(self):
+        return self.layers[0].t
+
+    def eager(self, stream=None):
+        t0 = self._shared()
+        L0 = self.layers[0]
+        tv_build_tree_mask(self.dims, t0["parents"], t0["anc"], t0["depth"], t0["row_status"], stream)
+        for r in self.layers:
+            t = r.t
+            tv_branch_compress(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["gate_w"], t["scr_c4"],
+                               t["scr_c128"], t0["row_status"], stream)
+            tv_verify_attention(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["scr_c4"], t["scr_c128"],
+                                t["q"], t["q_idx"], t["w_idx"], t["out"], t["lse"], t["sel"], t0["row_status"],
+                                t["workspace"], stream)
+        if "target_logits" in t0:
+            tv_select_accepted_path(self.dims, t0["parents"], t0["anc"], t0["depth"], t0["draft_tokens"],
+                                    t0["target_logits"], L0.vocab, t0["target_tokens"], t0["accepted_last"],
+                                    t0["next_token"], t0["row_status"], t0["select_ws"], stream)
+        for r in self.layers:
+            t = r.t
+            tv_commit_accepted_path(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["scr_c4"],
+                                    t["scr_c128"], t0["accepted_last"], t0["accept_nodes"], t0["accept_len"],
+                                    t0["row_status"], stream)
+
+    def capture(self) -> int:
+        """Record the round into a graph; returns the number of kernels in it."""
+        t0 = self._shared()
+        layers = (TvLayer * len(self.layers))()
+        for k, r in enumerate(self.layers):
+            t = r.t
+            layers[k] = TvLayer(r.cache, _ptr(t["tree_u"]), _ptr(t["gate_w"]), _ptr(t["q"]), _ptr(t["q_idx"]),
+                                _ptr(t["w_idx"]), _ptr(t["scr_c4"]), _ptr(t["scr_c128"]), _ptr(t["out"]),
+                                _ptr(t["lse"]), _ptr(t["sel"]), _ptr(t["workspace"]), _nbytes(t["workspace"]))
+        sel = "target_logits" in t0
+        rnd = TvRound(_ptr(t0["parents"]), _ptr(t0["anc"]), _ptr(t0["depth"]), _ptr(t0["row_status"]),
+                      _ptr(t0["accepted_last"]), _ptr(t0["accept_nodes"]), _ptr(t0["accept_len"]),
+                      _ptr(t0["draft_tokens"]) if sel else None, _ptr(t0["target_logits"]) if sel else None,
+                      self.layers[0].vocab if sel else 0, _ptr(t0["target_tokens"]) if sel else None,
+                      _ptr(t0["next_token"]) if sel else None, _ptr(t0["select_ws"]) if sel else None,
+                      _nbytes(t0["select_ws"]) if sel else 0)
+        self._keep = (layers, rnd)
+        h = ctypes.c_void_p()
+        _check(lib().tv_round_graph_create(ctypes.byref(self.dims), ctypes.byref(rnd), layers, len(self.layers),
+                                           ctypes.byref(h)), "tv_round_graph_create")
+        self.release()
+        self.graph = h
+        return int(lib().tv_round_graph_kernels(h))
+
+    def replay(self, stream=None):
+        if self.graph is None:
+            raise RuntimeError("capture() first")
+        _check(lib().tv_round_graph_launch(self.graph, _stream(stream)), "tv_round_graph_launch")
+
+    def release(self):
+        if self.graph is not None:
+            _check(lib().tv_round_graph_destroy(self.graph), "tv_round_graph_destroy")
+            self.graph = None
+
+    def __del__(self):
+        try:
+            self.release()
+        except Exception:
+            pass

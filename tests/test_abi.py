@@ -131,3 +131,26 @@ def test_select_arguments_checked_without_gpu():
     odd = list(args)
     odd[10] = ctypes.c_void_p((1 << 20) + 16)
     assert lib.tv_select_accepted_path(ctypes.byref(d), *odd, None) == binding.TV_ERR_INVALID_ARG
+
+
+def test_round_graph_arguments_checked_without_gpu():
+    lib = binding.lib()
+    d = _dims()
+    rnd = binding.TvRound()
+    layers = (binding.TvLayer * 2)()
+    h = ctypes.c_void_p(123)
+    assert lib.tv_round_graph_create(ctypes.byref(d), ctypes.byref(rnd), layers, 2, None) == binding.TV_ERR_INVALID_ARG
+    for n in (0, -1, 1025):
+        assert lib.tv_round_graph_create(ctypes.byref(d), ctypes.byref(rnd), layers, n, ctypes.byref(h)) == \
+            binding.TV_ERR_INVALID_ARG
+        assert h.value is None  # cleared on failure
+        h = ctypes.c_void_p(123)
+    assert lib.tv_round_graph_create(ctypes.byref(_dims(B=0)), ctypes.byref(rnd), layers, 2, ctypes.byref(h)) == \
+        binding.TV_ERR_INVALID_ARG
+    assert lib.tv_round_graph_create(ctypes.byref(d), None, layers, 2, ctypes.byref(h)) == binding.TV_ERR_INVALID_ARG
+    rnd.draft_tokens = 1 << 20  # selection inputs without logits
+    assert lib.tv_round_graph_create(ctypes.byref(d), ctypes.byref(rnd), layers, 2, ctypes.byref(h)) == \
+        binding.TV_ERR_INVALID_ARG
+    assert lib.tv_round_graph_launch(None, None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_round_graph_destroy(None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_round_graph_kernels(None) == 0
