@@ -106,8 +106,11 @@ typedef struct {
 } tv_dims;
 
 /* Committed (persistent) state of every row.  Only tv_commit_accepted_path
- * writes it; compress and verify only read it (Sec. 4.2: speculative branch
- * state never touches the persistent cache before acceptance). */
+ * writes its committed part; verify only reads it (Sec. 4.2: speculative
+ * branch state never touches the persistent cache before acceptance).  The
+ * one exception is the refresh schedule of tv_branch_compress with a
+ * designated chain, which writes CSA pool slots past the committed entries:
+ * slots no call reads until a commit makes them committed. */
 typedef struct {
   uint16_t *ring;   /* [B][ring_cap][d_row + d_idx]: raw row of position q in slot q & (ring_cap-1) */
   uint16_t *c4;     /* [*][d_row]: CSA entry s of row b at c4[c4_base[b] + s], s < len/ratio_csa */
@@ -139,11 +142,17 @@ tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64
  * written.
  *   tree_u   [B][D][d_row + d_idx] raw rows of the draft tokens, read
  *   gate_w   [2][d_row + d_idx] gate vectors for ratio_csa then ratio_hca, read
- *   row_status in/out: a row with len outside [0, max_len] becomes TV_ROW_BAD_LEN */
+ *   row_status in/out: a row with len outside [0, max_len] becomes TV_ROW_BAD_LEN
+ *   primary_last  int32 [B] or NULL.  Refresh schedule (Sec. 4.3): the root
+ *            path of primary_last[b] is the row's designated chain (say, the
+ *            drafter's first choice); the CSA entries its nodes close are also
+ *            written to their pool slots c4/c4_idx[c4_base[b] + s], s =
+ *            (p+1)/ratio_csa - 1, when s < c4_cap[b].  A value outside [0, D)
+ *            designates no chain.  Pass the same array to the commit. */
 tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
                              const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w,
                              uint16_t *scr_c4, uint16_t *scr_c128, int32_t *row_status,
-                             hipStream_t stream);
+                             const int32_t *primary_last, hipStream_t stream);
 
 /* Bytes of device workspace tv_verify_attention needs for these dims (the
  * largest row is bounded by dims->max_len).  0 on invalid dims. */
@@ -178,12 +187,21 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
  * A row that fails a check (accept index, pool capacity) is left untouched and
  * gets the row status.
  *   parents, depth, anc: as produced by tv_build_tree_mask (read)
- *   accepted_last int32 [B], accept_nodes int32 [B][D], accept_len int32 [B] */
+ *   accepted_last int32 [B], accept_nodes int32 [B][D], accept_len int32 [B]
+ *   primary_last  int32 [B] or NULL: the designated chains given to
+ *            tv_branch_compress.  CSA copies of accepted nodes on a row's
+ *            designated chain are skipped (the compression put them in
+ *            place): a single chain, or an accepted path that is the cached
+ *            chain, needs no CSA refresh (Sec. 4.3).  HCA entries are always
+ *            written here, after the path is known (Sec. 4.3: C128 writes
+ *            delayed and combined).  The committed state is the same as
+ *            without a designated chain. */
 tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const uint16_t *tree_u,
                                   const uint64_t *anc, const int32_t *depth,
                                   const uint16_t *scr_c4, const uint16_t *scr_c128,
                                   const int32_t *accepted_last, int32_t *accept_nodes,
-                                  int32_t *accept_len, int32_t *row_status, hipStream_t stream);
+                                  int32_t *accept_len, int32_t *row_status,
+                                  const int32_t *primary_last, hipStream_t stream);
 
 /* Bytes of device workspace tv_select_accepted_path needs for these dims and
  * vocabulary size.  0 on invalid dims or vocab < 1. */
@@ -252,6 +270,7 @@ typedef struct {
   const int32_t *parents;
   uint64_t *anc;
   int32_t *depth, *row_status, *accepted_last, *accept_nodes, *accept_len;
+  const int32_t *primary_last;     /* designated chains, or NULL (see tv_branch_compress) */
   const int32_t *draft_tokens;     /* selection inputs (may be NULL together) */
   const uint16_t *target_logits;
   int32_t vocab;

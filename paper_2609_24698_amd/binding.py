@@ -51,8 +51,8 @@ class TvLayer(ctypes.Structure):
 
 class TvRound(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
-        "parents", "anc", "depth", "row_status", "accepted_last", "accept_nodes", "accept_len", "draft_tokens",
-        "target_logits")] + [("vocab", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in (
+        "parents", "anc", "depth", "row_status", "accepted_last", "accept_nodes", "accept_len", "primary_last",
+        "draft_tokens", "target_logits")] + [("vocab", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in (
             "target_tokens", "next_token", "select_workspace")] + [("select_workspace_bytes", ctypes.c_size_t)]
 
 
@@ -74,11 +74,11 @@ def lib() -> ctypes.CDLL:
         dp = ctypes.POINTER(TvDims)
         cp = ctypes.POINTER(TvCache)
         L.tv_build_tree_mask.argtypes = [dp, vp, vp, vp, vp, vp]
-        L.tv_branch_compress.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tv_branch_compress.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tv_verify_workspace_bytes.argtypes = [dp]
         L.tv_verify_workspace_bytes.restype = sz
         L.tv_verify_attention.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
-        L.tv_commit_accepted_path.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tv_commit_accepted_path.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tv_select_workspace_bytes.argtypes = [dp, i32]
         L.tv_select_workspace_bytes.restype = sz
         L.tv_select_accepted_path.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
@@ -144,10 +144,11 @@ def tv_build_tree_mask(dims: TvDims, parents, anc, depth, row_status, stream=Non
 
 
 def tv_branch_compress(dims: TvDims, cache: TvCache, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status,
-                       stream=None) -> None:
+                       primary_last=None, stream=None) -> None:
     _check(lib().tv_branch_compress(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u), _ptr(anc, torch.int64),
                                     _ptr(depth, torch.int32), _ptr(gate_w), _ptr(scr_c4), _ptr(scr_c128),
-                                    _ptr(row_status, torch.int32), _stream(stream)),
+                                    _ptr(row_status, torch.int32), _ptr(primary_last, torch.int32),
+                                    _stream(stream)),
            "tv_branch_compress")
 
 
@@ -166,12 +167,13 @@ def tv_verify_attention(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4
 
 
 def tv_commit_accepted_path(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
-                            accept_nodes, accept_len, row_status, stream=None) -> None:
+                            accept_nodes, accept_len, row_status, primary_last=None, stream=None) -> None:
     _check(lib().tv_commit_accepted_path(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u),
                                          _ptr(anc, torch.int64), _ptr(depth, torch.int32), _ptr(scr_c4),
                                          _ptr(scr_c128), _ptr(accepted_last, torch.int32),
                                          _ptr(accept_nodes, torch.int32), _ptr(accept_len, torch.int32),
-                                         _ptr(row_status, torch.int32), _stream(stream)),
+                                         _ptr(row_status, torch.int32), _ptr(primary_last, torch.int32),
+                                         _stream(stream)),
            "tv_commit_accepted_path")
 
 
@@ -261,10 +263,18 @@ class DeviceRound:
         t = self.t
         tv_build_tree_mask(self.dims, t["parents"], t["anc"], t["depth"], t["row_status"], stream)
 
+    def set_primary(self, primary_last):
+        """Designate a chain per row (the refresh schedule of compress and
+        commit); None goes back to the plain refresh."""
+        if primary_last is None:
+            self.t.pop("primary_last", None)
+        else:
+            self.t["primary_last"] = _dev(np.asarray(primary_last, dtype=np.int32), self.t["parents"].device)
+
     def compress(self, stream=None):
         t = self.t
         tv_branch_compress(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["gate_w"], t["scr_c4"],
-                           t["scr_c128"], t["row_status"], stream)
+                           t["scr_c128"], t["row_status"], t.get("primary_last"), stream)
 
     def verify(self, stream=None, with_sel: bool = True, with_lse: bool = True):
         t = self.t
@@ -276,7 +286,7 @@ class DeviceRound:
         t = self.t
         tv_commit_accepted_path(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"],
                                 t["scr_c128"], t["accepted_last"], t["accept_nodes"], t["accept_len"],
-                                t["row_status"], stream)
+                                t["row_status"], t.get("primary_last"), stream)
 
     def attach_selection(self, sel, fill: int = -2):
         """Upload the draft tokens and target logits of ``sel`` (a synth
@@ -350,7 +360,7 @@ class LayeredRound:
         for r in self.layers:
             t = r.t
             tv_branch_compress(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["gate_w"], t["scr_c4"],
-                               t["scr_c128"], t0["row_status"], stream)
+                               t["scr_c128"], t0["row_status"], t0.get("primary_last"), stream)
             tv_verify_attention(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["scr_c4"], t["scr_c128"],
                                 t["q"], t["q_idx"], t["w_idx"], t["out"], t["lse"], t["sel"], t0["row_status"],
                                 t["workspace"], stream)
@@ -362,7 +372,7 @@ class LayeredRound:
             t = r.t
             tv_commit_accepted_path(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["scr_c4"],
                                     t["scr_c128"], t0["accepted_last"], t0["accept_nodes"], t0["accept_len"],
-                                    t0["row_status"], stream)
+                                    t0["row_status"], t0.get("primary_last"), stream)
 
     def capture(self) -> int:
         """Record the round into a graph; returns the number of kernels in it."""
@@ -376,6 +386,7 @@ class LayeredRound:
         sel = "target_logits" in t0
         rnd = TvRound(_ptr(t0["parents"]), _ptr(t0["anc"]), _ptr(t0["depth"]), _ptr(t0["row_status"]),
                       _ptr(t0["accepted_last"]), _ptr(t0["accept_nodes"]), _ptr(t0["accept_len"]),
+                      _ptr(t0.get("primary_last"), torch.int32),
                       _ptr(t0["draft_tokens"]) if sel else None, _ptr(t0["target_logits"]) if sel else None,
                       self.layers[0].vocab if sel else 0, _ptr(t0["target_tokens"]) if sel else None,
                       _ptr(t0["next_token"]) if sel else None, _ptr(t0["select_ws"]) if sel else None,

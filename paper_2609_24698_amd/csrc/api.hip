@@ -194,16 +194,18 @@ tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64
 
 tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
                              const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4,
-                             uint16_t *scr_c128, int32_t *row_status, hipStream_t stream) {
+                             uint16_t *scr_c128, int32_t *row_status, const int32_t *primary_last,
+                             hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
   if (!cache_complete(cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
     return TV_ERR_INVALID_ARG;
-  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status))
+  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status) ||
+      (primary_last && !a16(primary_last)))
     return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("branch_compress", launch_compress(*dims, view(*cache), tree_u, anc, depth, gate_w, scr_c4, scr_c128,
-                                               row_status, stream));
+                                               row_status, primary_last, cache->c4, cache->c4_idx, stream));
   return TV_OK;
 }
 
@@ -253,18 +255,19 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
 tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const uint16_t *tree_u, const uint64_t *anc,
                                   const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                                   const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
-                                  int32_t *row_status, hipStream_t stream) {
+                                  int32_t *row_status, const int32_t *primary_last, hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
   if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
       !accept_nodes || !accept_len || !row_status)
     return TV_ERR_INVALID_ARG;
   if (!cache_a16(cache) ||
-      !all_a16(tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes, accept_len, row_status))
+      !all_a16(tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes, accept_len, row_status) ||
+      (primary_last && !a16(primary_last)))
     return TV_ERR_INVALID_ARG;
   if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("commit_path", launch_commit(*dims, *cache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
-                                         accept_nodes, accept_len, row_status, stream));
+                                         accept_nodes, accept_len, row_status, primary_last, stream));
   return TV_OK;
 }
 
@@ -314,7 +317,8 @@ static tv_status record_round(const tv_dims *d, const tv_round &r, const tv_laye
   tv_status st = tv_build_tree_mask(d, r.parents, r.anc, r.depth, r.row_status, s);
   for (int l = 0; l < n && st == TV_OK; ++l) {
     const tv_layer &L = layers[l];
-    st = tv_branch_compress(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status, s);
+    st = tv_branch_compress(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status,
+                            r.primary_last, s);
     if (st != TV_OK) break;
     st = tv_verify_attention(d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx,
                              L.out, L.lse, L.sel, r.row_status, L.workspace, L.workspace_bytes, s);
@@ -326,7 +330,7 @@ static tv_status record_round(const tv_dims *d, const tv_round &r, const tv_laye
   for (int l = 0; l < n && st == TV_OK; ++l) {
     tv_cache c = layers[l].cache;
     st = tv_commit_accepted_path(d, &c, layers[l].tree_u, r.anc, r.depth, layers[l].scr_c4, layers[l].scr_c128,
-                                 r.accepted_last, r.accept_nodes, r.accept_len, r.row_status, s);
+                                 r.accepted_last, r.accept_nodes, r.accept_len, r.row_status, r.primary_last, s);
   }
   return st;
 }

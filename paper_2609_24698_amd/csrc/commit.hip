@@ -8,6 +8,13 @@
 //
 // One workgroup per row.  All checks run before the first write, so a failing
 // row is left exactly as it was.
+//
+// Refresh schedule (Sec. 4.3): with a designated chain (the root path of
+// primary_last[b]), whose CSA entries the compression already wrote into the
+// pool, the CSA copies of accepted nodes on that chain are skipped: a single
+// chain, or an accepted path that is the cached chain, needs no CSA refresh.
+// HCA entries are always written here, once the path is known, all of a
+// round's in one pass.
 #include "tv_common.h"
 #include "tv_internal.h"
 
@@ -21,7 +28,8 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
                                                      const int32_t *__restrict__ accepted_last,
                                                      int32_t *__restrict__ accept_nodes,
                                                      int32_t *__restrict__ accept_len,
-                                                     int32_t *__restrict__ row_status) {
+                                                     int32_t *__restrict__ row_status,
+                                                     const int32_t *__restrict__ primary_last) {
   __shared__ int32_t path[64];
   const int b = blockIdx.x, tid = threadIdx.x;
   if (row_status[b] != TV_ROW_OK) return;
@@ -31,11 +39,13 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
     return;
   }
   const int32_t last = accepted_last[b];
+  const int32_t P = primary_last ? primary_last[b] : -1;
   if (last < 0 || last >= d.D) {
     if (tid == 0) row_status[b] = TV_ROW_BAD_ACCEPT;
     return;
   }
   const uint64_t m = anc[(int64_t)b * d.D + last];
+  const uint64_t chain = (P >= 0 && P < d.D) ? anc[(int64_t)b * d.D + P] : 0ull;
   const int a = depth[(int64_t)b * d.D + last] + 1;
   if (tid < d.D && ((m >> tid) & 1ull)) path[depth[(int64_t)b * d.D + tid]] = tid;
   bool bad = false;
@@ -61,7 +71,7 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
   for (int t = 0; t < a; ++t) {
     const int64_t p = (int64_t)L + t;
     const int j = path[t];
-    if ((p + 1) % d.ratio_csa == 0) {
+    if ((p + 1) % d.ratio_csa == 0 && !((chain >> j) & 1ull)) {
       const int64_t slot = c.c4_base[b] + (p + 1) / d.ratio_csa - 1;
       const uint16_t *src = scr_c4 + ((int64_t)b * d.D + j) * d_u;
       for (int e = tid; e < d_u / 8; e += blockDim.x) {
@@ -90,9 +100,9 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
 hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
                          const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                          const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
-                         int32_t *row_status, hipStream_t s) {
+                         int32_t *row_status, const int32_t *primary_last, hipStream_t s) {
   commit_kernel<<<d.B, 256, 0, s>>>(d, c, tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes,
-                                    accept_len, row_status);
+                                    accept_len, row_status, primary_last);
   return hipGetLastError();
 }
 

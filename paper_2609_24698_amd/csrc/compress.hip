@@ -16,6 +16,12 @@
 // block in one pass) and the weighted sums (8 token groups per 16-byte channel
 // chunk) stream them with 16-byte loads, all of a thread's loads in flight
 // together.
+//
+// Refresh schedule (Sec. 4.3): when the caller designates a chain (the root
+// path of primary_last[b]), the CSA entries its nodes close are also written
+// straight into their persistent pool slots.  Those slots lie past the
+// committed entries, so nothing reads them before the commit makes them
+// committed, and the commit then skips their copies.
 #include "tv_common.h"
 #include "tv_internal.h"
 
@@ -37,13 +43,16 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
                                                        const int32_t *__restrict__ depth,
                                                        const uint16_t *__restrict__ gate_w,
                                                        uint16_t *__restrict__ scr_c4, uint16_t *__restrict__ scr_c128,
-                                                       int32_t *__restrict__ row_status) {
+                                                       int32_t *__restrict__ row_status,
+                                                       const int32_t *__restrict__ primary_last,
+                                                       uint16_t *__restrict__ pool_c4, uint16_t *__restrict__ pool_c4_idx) {
   __shared__ int32_t path[64];
   __shared__ const uint16_t *tok[kMaxRatio];
   __shared__ float wgt[2][kMaxRatio];
   __shared__ float gate[2][kMaxDu];
   __shared__ float part[2][kMaxGroups][kMaxDu];
   __shared__ float red[2][2];
+  __shared__ uint64_t chain_sh;
   const int b = blockIdx.x / d.D;
   const int i = blockIdx.x - b * d.D;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -55,6 +64,11 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   const int32_t dep = depth[node];
   const uint64_t m = anc[node];
   const int32_t dj = tid < d.D ? depth[(int64_t)b * d.D + tid] : 0;
+  const uint64_t aj = (primary_last && tid < d.D) ? anc[(int64_t)b * d.D + tid] : 0ull;
+  const int32_t P = primary_last ? primary_last[b] : -1;
+  const int32_t cap4 = primary_last ? c.c4_cap[b] : 0;
+  const int64_t base4 = primary_last ? c.c4_base[b] : 0;
+  asm volatile("" ::"s"(cap4), "s"(base4));  // issued with the other loads
   const float g0 = tid < d_u ? bf2f(gate_w[tid]) : 0.f;
   const float g1 = tid < d_u ? bf2f(gate_w[d_u + tid]) : 0.f;
   asm volatile("" ::"v"(g0), "v"(g1));  // gate loads issued with the others, not after the checks
@@ -73,6 +87,10 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   const int R = std::max(cl[0] ? rat[0] : 0, cl[1] ? rat[1] : 0);
   const int first[2] = {R - rat[0], R - rat[1]};
   if (tid < d.D && ((m >> tid) & 1ull)) path[dj] = tid;
+  if (wv == 0) {  // the designated chain: ancestor mask of node P (lane P holds it), empty if none
+    const uint64_t ap = __shfl(aj, (P >= 0 && P < d.D) ? P : 0, 64);
+    if (tid == 0) chain_sh = (P >= 0 && P < d.D) ? ap : 0ull;
+  }
   if (tid < d_u) {
     gate[0][tid] = g0;
     gate[1][tid] = g1;
@@ -188,6 +206,10 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
     }
   }
   __syncthreads();
+  // a CSA entry closed on the designated chain also goes to its pool slot, capacity permitting
+  const int64_t slot4 = (p + 1) / d.ratio_csa - 1;
+  const bool through = cl[0] && ((chain_sh >> i) & 1ull) && slot4 < cap4;
+  const int64_t pslot = base4 + slot4;
 #pragma unroll
   for (int ri = 0; ri < 2; ++ri) {
     if (!cl[ri]) continue;
@@ -196,17 +218,26 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
       float sum = 0.f;
 #pragma unroll
       for (int gg = 0; gg < G; ++gg) sum += part[ri][gg][ch];  // group order
-      dst[ch] = f2bf(sum);
+      const uint16_t v = f2bf(sum);
+      dst[ch] = v;
+      if (ri == 0 && through) {
+        if (ch < d.d_row)
+          pool_c4[pslot * d.d_row + ch] = v;
+        else
+          pool_c4_idx[pslot * d.d_idx + (ch - d.d_row)] = v;
+      }
     }
   }
 }
 
 hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                            const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4, uint16_t *scr_c128,
-                           int32_t *row_status, hipStream_t s) {
+                           int32_t *row_status, const int32_t *primary_last, uint16_t *pool_c4,
+                           uint16_t *pool_c4_idx, hipStream_t s) {
   if (d.d_row + d.d_idx > kMaxDu) return hipErrorInvalidValue;
   dim3 grid(d.B * d.D);
-  compress_kernel<<<grid, kNT, 0, s>>>(d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status);
+  compress_kernel<<<grid, kNT, 0, s>>>(d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status, primary_last,
+                                       pool_c4, pool_c4_idx);
   return hipGetLastError();
 }
 

@@ -48,7 +48,8 @@ hipError_t launch_mask(const tv_dims &d, const int32_t *parents, uint64_t *anc, 
                        int32_t *row_status, hipStream_t s);
 hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                            const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4, uint16_t *scr_c128,
-                           int32_t *row_status, hipStream_t s);
+                           int32_t *row_status, const int32_t *primary_last, uint16_t *pool_c4,
+                           uint16_t *pool_c4_idx, hipStream_t s);
 hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
                         const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s);
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
@@ -64,7 +65,7 @@ hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int
 hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
                          const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                          const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
-                         int32_t *row_status, hipStream_t s);
+                         int32_t *row_status, const int32_t *primary_last, hipStream_t s);
 
 // Accepted-path selection: chunk keys of the target argmax, then the greedy path.
 int select_chunks(int32_t vocab);

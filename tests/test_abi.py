@@ -58,8 +58,9 @@ def test_null_pointers_rejected_without_gpu():
     d = _dims()
     assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == binding.TV_ERR_INVALID_ARG
     cache = binding.TvCache()
-    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([None] * 8)) == binding.TV_ERR_INVALID_ARG
-    assert lib.tv_commit_accepted_path(ctypes.byref(d), ctypes.byref(cache), *([None] * 10)) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([None] * 9)) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_commit_accepted_path(ctypes.byref(d), ctypes.byref(cache), *([None] * 11)) == \
+        binding.TV_ERR_INVALID_ARG
     assert lib.tv_verify_attention(ctypes.byref(d), ctypes.byref(cache), *([None] * 13), 0, None) == \
         binding.TV_ERR_INVALID_ARG
 
@@ -95,7 +96,14 @@ def test_misaligned_pointers_rejected_without_gpu():
     for name, _ in binding.TvCache._fields_:
         setattr(cache, name, ok.value)
     cache.c4_idx = bad.value
-    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([ok] * 7), None) == \
+    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([ok] * 7), None, None) == \
+        binding.TV_ERR_INVALID_ARG
+    for name, _ in binding.TvCache._fields_:
+        setattr(cache, name, ok.value)
+    # the optional designated chains must be aligned too
+    assert lib.tv_branch_compress(ctypes.byref(d), ctypes.byref(cache), *([ok] * 7), bad, None) == \
+        binding.TV_ERR_INVALID_ARG
+    assert lib.tv_commit_accepted_path(ctypes.byref(d), ctypes.byref(cache), *([ok] * 9), bad, None) == \
         binding.TV_ERR_INVALID_ARG
 
 
