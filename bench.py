@@ -14,7 +14,9 @@ stream around every kernel during K further timed steps); and the CPU oracle
 timed on a bounded sample of the same workload.  Under "next_rows" it adds the
 greedy accepted-path selection over the same trees (target argmax over a
 129,280-token vocabulary at every node, then the path), timed on its own with
-the roofline of its argmax kernel, and a round over 61 layers (DeepSeek-V3's
+the roofline of its argmax kernel; the refresh schedule (compress and commit
+with each row's accepted path designated as its cached chain, against the
+plain refresh); and a round over 61 layers (DeepSeek-V3's
 depth; the paper does not state V4-Flash's) issued call by call against the
 same round replayed as one HIP graph; neither is part of the step.
 """
@@ -139,7 +141,7 @@ def bench_workload(config: str, steps: int, warmup: int, seed=None):
     for every step's commit (at most D tokens per row per step)."""
     import synth
 
-    grow = (2 * steps + warmup + 2) * synth.CONFIGS[config]["D"]
+    grow = (3 * steps + warmup + 2) * synth.CONFIGS[config]["D"]  # three timed regions of K steps
     return synth.make_workload(config, seed=seed, max_len_margin=grow, extra_c4=grow // 4 + 8,
                                extra_c128=grow // 128 + 4)
 
@@ -190,6 +192,27 @@ def time_selection(r, wl, K, binding, torch):
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                          "traffic": None, "algorithmic_bytes_per_launch": int(a_bytes),
                          "avg_launch_ms": round(avg, 5)}}
+
+
+def time_refresh(r, wl, K, binding, torch, plain_kern):
+    """The refresh schedule with every row's accepted path designated as its
+    cached chain (the case where the CSA refresh is skipped entirely): K more
+    whole steps with per-kernel HIP events, against the plain steps."""
+    r.set_primary(wl.accepted_last)
+    binding.tv_profile_enable(8 * K + 16)
+    for _ in range(K):
+        r.round()
+    torch.cuda.synchronize()
+    kern = binding.tv_profile_read()
+    binding.tv_profile_disable()
+    r.set_primary(None)
+    status = r.host("row_status")
+    assert np.all(status == 0), f"rows left the workload: {np.unique(status)}"
+    out = {}
+    for k in ("branch_compress", "commit_path"):
+        out[k] = {"plain_ms": round(plain_kern[k][1] / plain_kern[k][0], 4),
+                  "designated_chain_ms": round(kern[k][1] / kern[k][0], 4)}
+    return out
 
 
 def time_graph(config: str, n_layers: int, K: int, W: int, torch):
@@ -373,13 +396,13 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(a_bytes), "avg_launch_ms": round(avg_ms, 5)},
     }
+    refresh = time_refresh(r, wl, K, binding, torch, kern)
     graph = None
     if not args.no_graph:
         graph = {"workloads": {}}
         for cfg in dict.fromkeys([args.config, "C1"]):
             graph["workloads"][cfg] = time_graph(cfg, args.graph_layers, K, W, torch)
-    if select is not None or graph is not None:
-        res["next_rows"] = {}
+    res["next_rows"] = {"refresh_schedule": refresh}
     if select is not None:
         res["next_rows"]["select_accepted_path"] = select
         print(f"[bench] selection: {select['ms_per_call']:.4f} ms per call, argmax "
