@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 METRIC = "verified tree tokens/sec at B=64,D=8,16K ctx; % of MI355X peak HBM GB/s"
 HBM_PEAK_GBS = 8000.0
 DOMINANT = "verify_attn"
-KERNEL_SOURCES = {"verify_attn": ["attn.hip", "node_keys.h", "tv_common.h"],
+KERNEL_SOURCES = {"verify_attn": ["attn_mla.hip", "attn_common.h", "tv_common.h"],
                   "target_argmax": ["select.hip", "tv_common.h"]}
 
 WORKLOADS = {

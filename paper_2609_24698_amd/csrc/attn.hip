@@ -24,18 +24,9 @@
 // combine kernel merges in split order.
 #include <algorithm>
 
-#include "tv_common.h"
-#include "tv_internal.h"
+#include "attn_common.h"
 
 namespace tv {
-
-constexpr int kKT = 32;          // keys per tile
-constexpr int kMaxChunk = kAttnMaxChunk;  // keys per split (pointer table in LDS)
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-typedef __attribute__((ext_vector_type(4))) short i16x4;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 struct AttnShape {
@@ -70,48 +61,6 @@ struct AttnShape {
     return (r * CPR + (c & ~7) + ((c & 7) ^ swz(r))) * 16 + (col & 7) * 2;
   }
 };
-
-// Decode the XCD-aware block index.  Workgroups are dealt to the 8 XCDs
-// round-robin and each XCD starts its workgroups in order, so rows are dealt
-// to XCDs in the order row_order gives (longest first): every unit of the
-// row of rank rho runs on XCD rho % 8, where the row's shared HCA, window and
-// overlapping CSA entries stay in one L2, and each XCD starts its longest
-// rows first.  Returns the rank; b is valid when the rank is below B.
-__device__ __forceinline__ int unit_of(int blk, int D, int splits, int &i, int &s) {
-  const int x = blk & 7, q = blk >> 3;
-  s = q % splits;
-  const int r = q / splits;
-  i = r % D;
-  return (r / D) * 8 + x;
-}
-
-// Barrier that waits for this wavefront's LDS traffic only: global loads in
-// flight (the next tiles) stay in flight across it.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-template <int N>
-__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
-
-// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
-// lane l's 16 bytes land at LDS byte address lds + 16 l.  Issued from inline
-// assembly so that the compiler's wait-count pass does not order later LDS
-// reads of other buffers behind it; completion is awaited explicitly with
-// vm_wait<> before the barrier that publishes the tile (both carry memory
-// clobbers, the copy itself needs none: nothing reads its destination before
-// that barrier).  M0 (the LDS base) is saved and restored around the copy.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds)));
-}
-
-typedef __attribute__((ext_vector_type(2))) float f32x2;
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
 __global__ void __launch_bounds__(NW * 64, 1)
@@ -579,8 +528,7 @@ hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_s
                        const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
                        float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
   if (d.H == 64 && d.d_k == 576 && d.d_v == 512 && d.v_off == 0 && d.d_row == 576)
-    return launch_attn_t<8, 2, 576, 512, 0, 576>(d, q, row_status, row_order, keytab, nkeys, plan, part_o, part_ml,
-                                                 out, lse, s);
+    return launch_attn_mla(d, q, row_status, row_order, keytab, nkeys, plan, part_o, part_ml, out, lse, s);
   if (d.H == 8 && d.d_k == 128 && d.d_v == 128 && d.v_off == 128 && d.d_row == 256)
     return launch_attn_t<4, 1, 128, 128, 128, 256>(d, q, row_status, row_order, keytab, nkeys, plan, part_o,
                                                    part_ml, out, lse, s);

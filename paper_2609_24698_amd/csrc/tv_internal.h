@@ -60,6 +60,9 @@ hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tre
 hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
                        const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
                        float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+hipError_t launch_attn_mla(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
+                           const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
+                           float *part_ml, uint16_t *out, float *lse, hipStream_t s);
 hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s);
 hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
