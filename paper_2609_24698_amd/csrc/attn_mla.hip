@@ -2,38 +2,33 @@
 // over one 576-wide latent row per key; keys are the whole row, values its
 // first 512 channels.
 //
-// One workgroup (8 wavefronts, two per SIMD) takes one (row, node, key
-// split).  A 32-key tile is gathered once into LDS (direct global->LDS
-// copies) and feeds two contractions on MFMA, float32 accumulation:
-//   S^T = K Q^T     keys x heads, v_mfma_f32_16x16x32_bf16.  Wave (head
-//                   quarter hq, key half kh) computes the complete logits of
-//                   heads 16hq..16hq+15 against keys 16kh..16kh+15 over all
-//                   576 channels (its queries stay in registers), so no
-//                   partial logits cross LDS.  It exponentiates them in
-//                   registers against a fixed per-head reference and
-//                   publishes bf16 P.
-//   O^T += V^T P^T  value channels x heads, v_mfma_f32_32x32x16_bf16.  Wave w
-//                   owns value channels 64w..64w+63 for all heads; V^T comes
-//                   from the LDS transpose read (ds_read_b64_tr_b16), each
-//                   value element once per tile.
-// The tile is stored group-major: column group g (64 channels, 128 bytes) of
-// all 32 rows, then group g+1, the 16-byte chunk slot XOR-swizzled by row
-// pair, which keeps both the logit reads (16 rows x one chunk) and the
-// transpose reads free of bank conflicts.  Wave w reads only group w of a
-// tile for its values, and every wave's logit reads of tile t end one barrier
-// before tile t's values are read, so wave w copies group w of tile t+3 (and
-// a quarter of the rope group, read by the logits only) into the buffer of
-// tile t right after its own P V reads: two iterations of lead, no barrier.
+// One workgroup (8 wavefronts) takes one (row, node, key split).  Wavefronts
+// w and w+4 share a SIMD, and w0..w3 occupy the four SIMDs, so the roles are:
+//   w0, w1  logit waves: S^T = K Q^T for 32 keys x 32 heads (head half w)
+//           over all 576 channels on v_mfma_f32_32x32x16_bf16, the queries of
+//           their 32 heads held in registers; they exponentiate against a
+//           fixed per-head reference and publish bf16 P^T.
+//   w2, w3, w6, w7  value waves: O^T += V^T P^T, 128 value channels each for
+//           all 64 heads (32x32x16, V^T from the LDS transpose read).
+//   w4, w5  copy waves: gather the key rows of tile t+3 into LDS with direct
+//           global->LDS copies (w4 also copies the key-pointer table of tile
+//           t+6), so a tile lands two iterations before its logits.
+// Per tile a logit SIMD issues 36 products and a value SIMD 32; nothing is
+// recomputed and no partial logits cross LDS.
 //
-// One barrier per tile: iteration t computes the logits and probabilities of
-// tile t+1 and the P V of tile t.  The probabilities use a fixed reference
-// per head (the first tile's maximum), so the output accumulators are never
-// rescaled; a logit more than 64 (log2 units) above it restarts the split
-// from the largest logit seen, at most kMaxRestarts times.
+// Iteration it (one barrier each, it = -1 .. T-1) computes the logits and
+// probabilities of tile it+1 and the P V of tile it.  K tiles live in four
+// LDS buffers (tile u in buffer u % 4), stored group-major: column group g
+// (64 channels, 128 bytes) of all 32 rows, then group g+1, the 16-byte chunk
+// slot XOR-swizzled by row pair, so that the logit reads (32 rows x one chunk)
+// and the transpose reads are free of bank conflicts.
 //
-// A node whose keys fit one split writes its normalised output; otherwise each
-// split writes an unnormalised partial (O, reference, sum) that the combine
-// kernel merges.
+// The probabilities use a fixed reference per head (the first tile's
+// maximum), so the output accumulators are never rescaled; a logit more than
+// 64 (log2 units) above it restarts the split from the largest logit seen,
+// at most kMaxRestarts times.  A node whose keys fit one split writes its
+// normalised output; otherwise each split writes an unnormalised partial
+// (O, reference, sum) that the combine kernel merges.
 #include "attn_common.h"
 
 namespace tv {
@@ -42,14 +37,17 @@ namespace mla {
 
 constexpr int kH = 64, kDK = 576, kDV = 512;
 constexpr int kNW = 8, kNT = kNW * 64;
-constexpr int kKS = kDK / 32;             // logit k-steps of 32 channels
+constexpr int kKS = kDK / 16;             // logit k-steps of 16 channels
 constexpr int kGroups = kDK / 64;         // 128-byte column groups of a row (the last one: rope channels)
 constexpr int kGB = kKT * 128;            // bytes of one column group of a tile
 constexpr int kTB = kGroups * kGB;        // bytes of a tile
-constexpr int kNBUF = 3;
-constexpr int kNPW = kKT * 128 / 1024 + 1;  // copy instructions per wave and tile: its group, then a rope quarter
-static_assert(kGroups == kNW + 1, "one value group per wave plus one rope group");
-static_assert(kDV == 64 * kNW, "wave w owns value channels 64w..64w+63");
+constexpr int kNBUF = 4;                  // K tile buffers
+constexpr int kPSlots = 8;                // key-pointer table slots (one tile each)
+constexpr int kG0 = 5;                    // column groups copied by w4 (w5 copies the rest)
+constexpr float kSlack = 64.0f;
+constexpr int kMaxRestarts = 8;
+static_assert(kDV == 128 * 4, "four value waves of 128 channels");
+static_assert(kGroups == 9, "eight value groups and one rope group");
 
 // 16-byte chunk slot of logical chunk `c` (0..7 within its group) in row r.
 __device__ constexpr int slot(int r, int c) { return c ^ ((r >> 1) & 7); }
@@ -62,11 +60,39 @@ __device__ constexpr int off(int r, int col) {
 // key 16s + 8a + 4h + i (s, a, h in {0,1}, i < 4) sits at 16s + 8h + 4a + i,
 // so the eight keys one lane of the value contraction needs (k-step s, lane
 // half h: keys 16s + 4h + 0..3, then 16s + 8 + 4h + 0..3) are one 16-byte
-// chunk; chunk slots are XOR-swizzled by head so a read of 32 heads spreads
-// over all banks.
+// chunk, and so are the eight logits one lane of the logit product holds for
+// that k-step.  Chunk slots are XOR-swizzled by head so that a read or write
+// of 32 heads spreads over all banks.
 __device__ constexpr int p_off(int head, int chunk) { return head * 64 + ((chunk ^ ((head >> 2) & 3)) * 16); }
 
 }  // namespace mla
+
+// Direct global -> LDS copy of 4 bytes per lane (global_load_lds_dword): lane
+// l's 4 bytes land at LDS byte address lds + 4 l.  Same protocol as dma16.
+__device__ __forceinline__ void dma4(const void *g, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds)));
+}
+
+// Wait until at most n of this wavefront's vector-memory operations are in
+// flight (n is one of the counts a copy wave issues per iteration).
+__device__ __forceinline__ void vm_wait_n(int n) {
+  switch (n) {
+    case 0: vm_wait<0>(); break;
+    case 1: vm_wait<1>(); break;
+    case 4 * (mla::kGroups - mla::kG0): vm_wait<4 * (mla::kGroups - mla::kG0)>(); break;
+    case 4 * mla::kG0: vm_wait<4 * mla::kG0>(); break;
+    case 4 * mla::kG0 + 1: vm_wait<4 * mla::kG0 + 1>(); break;
+    default: vm_wait<0>(); break;
+  }
+}
 
 __global__ void __launch_bounds__(mla::kNT, 1)
 attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict__ row_status,
@@ -76,9 +102,9 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   using namespace mla;
   __shared__ __attribute__((aligned(1024))) unsigned char sK[kNBUF][kTB];
   __shared__ __attribute__((aligned(16))) unsigned char sP[2][kH * 64];
-  __shared__ const uint16_t *sPtr[kMaxChunk];
-  __shared__ int sFlag[2][kNW];
-  __shared__ float sMx[2][kH];
+  __shared__ __attribute__((aligned(16))) const uint16_t *sPtr[kPSlots][kKT];
+  __shared__ int sFlag[2][2];
+  __shared__ float sSum[kH];
   __shared__ float sRef[kH];
 
   int i, split;
@@ -86,295 +112,281 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   if (rank >= d.B) return;
   const int b = row_order[rank];
   const int64_t node = (int64_t)b * d.D + i;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int hq = wv & 3, kh = wv >> 2;      // logit roles: head quarter, key half
-  const int l16 = lane & 15, g4 = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform role index
   const int l32 = lane & 31, hi = lane >> 5;
-  const int head = 16 * hq + l16;           // this lane's head in the logit roles
   const int k0 = split * chunk;
-  // Row status, key count, this thread's entries of the node's key table and
-  // the queries are loaded together; the table loads come first so that
-  // storing them waits for them only.
   const int32_t status = row_status[b];
   const int n_keys = nkeys_tab[node];
-  constexpr int kPer = (kMaxChunk + kNT - 1) / kNT;
-  const uint16_t *tp[kPer];
-  {
-    const uint16_t *const *tab = keytab + node * keytab_stride + k0;
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int t = tid + kNT * u;
-      tp[u] = (t < chunk && k0 + t < keytab_stride) ? tab[t] : nullptr;
-    }
-  }
-  // Queries as the B operand of the logits: lane holds head `head`, channels
-  // 32 ks + 8 g4 .. +7 of k-step ks.
-  bf16x8 qf[kKS];
-  {
-    const uint16_t *qrow = q + (node * kH + head) * kDK + 8 * g4;
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(qrow + 32 * ks));
-  }
   if (status != TV_ROW_OK || k0 >= n_keys) return;
-  const int k1 = std::min(n_keys, k0 + chunk);
-  const int nkeys = k1 - k0;
-  const int ntiles = (nkeys + kKT - 1) / kKT;
-#pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    const int t = tid + kNT * u;
-    if (t < nkeys) sPtr[t] = tp[u];
-  }
-  // Logit A operand: lane reads row 16 kh + l16, chunk 4 ks + g4, i.e. group
-  // ks/2, logical chunk 4 (ks & 1) + g4 of that group.
-  const int krow = 16 * kh + l16;
-  const int kbase[2] = {krow * 128 + slot(krow, g4) * 16, krow * 128 + slot(krow, 4 + g4) * 16};
-  // Value-operand offsets for the transpose reads: rows 16 ks + 8 s + 4 hi + jj/4,
-  // columns 64 wv + 16 (g & 1) + 4 (jj & 3) + 32 ct.
-  const int g = lane >> 4, jj = lane & 15;
-  int voff[4][2];
-#pragma unroll
-  for (int rr = 0; rr < 4; ++rr)
-#pragma unroll
-    for (int ct = 0; ct < 2; ++ct)
-      voff[rr][ct] = off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2), 64 * wv + 16 * (g & 1) + 4 * (jj & 3) + 32 * ct);
-  // P^T writes of this lane: keys 16 kh + 4 g4 + 0..3 of head `head`
-  const int pw = p_off(head, 2 * kh + (g4 & 1)) + (g4 >> 1) * 8;
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers before the loop
-  __syncthreads();                     // pointer table ready
-
-  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
-  // Source addresses of this wave's copies of a tile, read from the pointer
-  // table one phase ahead of the copies.  Instruction k < 4 fills rows
-  // 8k..8k+7 of group wv (lane = row-in-8 * 8 + slot); instruction 4 fills rows
-  // 4wv..4wv+3 of the rope group (lanes 0..31).  Slot s of row r holds logical
-  // chunk slot(r, s) of the group.  Rows past the split's end re-read its last
-  // key (finite data; their probabilities are forced to 0).
-  const unsigned char *nsrc[kNPW];
-  auto load_srcs = [&](int tile) {
-#pragma unroll
-    for (int k = 0; k < kNPW; ++k) {
-      const int s8 = lane & 7;
-      int r, c;
-      if (k < kNPW - 1) {
-        r = 8 * k + (lane >> 3);
-        c = 8 * wv + slot(r, s8);
-      } else {
-        r = 4 * wv + ((lane & 31) >> 3);
-        c = 8 * kNW + slot(r, s8);
-      }
-      const int t = std::min(tile * kKT + r, nkeys - 1);
-      nsrc[k] = reinterpret_cast<const unsigned char *>(sPtr[t]) + c * 16;
-    }
-  };
-  auto issue_tile = [&](int buf) {
-#pragma unroll
-    for (int k = 0; k < kNPW; ++k) {
-      if (k < kNPW - 1)
-        dma16(nsrc[k], lds_base + buf * kTB + wv * kGB + k * 1024);
-      else if (lane < 32)
-        dma16(nsrc[k], lds_base + buf * kTB + kNW * kGB + wv * 512);
-    }
-  };
-
-  f32x16 acc_o[2][2];
-  float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
+  const int nkeys = std::min(n_keys, k0 + chunk) - k0;
+  const int T = (nkeys + kKT - 1) / kKT;
+  const bool single = n_keys <= chunk;
   const float sl2 = d.scale * kLog2e;
-  constexpr float kSlack = 64.0f;
-  constexpr int kMaxRestarts = 8;
+  auto overflowed = [&](int it) { return (sFlag[it & 1][0] | sFlag[it & 1][1]) != 0; };
 
-  // Complete logits of this wave's 16 keys x 16 heads of tile `it`, two
-  // accumulator chains (even and odd k-steps), key reads kept four ahead.
-  auto qk_tile = [&](int it) {
-    const unsigned char *kt = sK[it % kNBUF];
-    f32x4 s0 = f32x4{}, s1 = f32x4{};
+  if (wv == 0 || wv == 1) {
+    // ---- logit wave: heads 32 hh .. 32 hh + 31 ------------------------------
+    const int hh = wv;
+    const int head = 32 * hh + l32;
+    // Queries as the B operand: lane holds head `head`, channels 16 ks + 8 hi .. +7.
+    bf16x8 qf[kKS];
+    {
+      const uint16_t *qrow = q + (node * kH + head) * kDK + 8 * hi;
 #pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + (ks >> 1) * kGB + kbase[ks & 1]);
-      if (ks & 1)
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], s1, 0, 0, 0);
-      else
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], s0, 0, 0, 0);
+      for (int ks = 0; ks < kKS; ++ks)
+        qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(qrow + 16 * ks));
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+    // A operand: lane reads row l32, chunk 2 (ks & 3) + hi of group ks / 4.
+    int kofs[4];
 #pragma unroll
-    for (int r = 0; r < kKS - 4; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int c = 0; c < 4; ++c) kofs[c] = l32 * 128 + slot(l32, 2 * c + hi) * 16;
+    const int pw0 = p_off(head, hi), pw1 = p_off(head, 2 + hi);
+
+    float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
+    // Complete logits of the tile's 32 keys x this wave's 32 heads: two
+    // accumulator chains (even and odd k-steps), key reads six ahead.
+    auto qk_tile = [&](int tile) {
+      const unsigned char *kt = sK[tile % kNBUF];
+      f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + (ks >> 2) * kGB + kofs[ks & 3]);
+        if (ks & 1)
+          s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s1, 0, 0, 0);
+        else
+          s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s0, 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+      for (int r = 0; r < kKS - 6; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+      return s0 + s1;
+    };
+    // Element v of a lane's logits is key 8 (v / 4) + 4 hi + v % 4 of the
+    // tile; keys past the split are -inf.
+    auto process = [&](int tile, f32x16 s, bool first) {
+      const int nvalid = nkeys - tile * kKT;
+      if (nvalid < kKT) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (8 * (v >> 2) + 4 * hi + (v & 3) >= nvalid) s[v] = -INFINITY;
+      }
+      float mx = s[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
+      mx *= sl2;
+      if (first) m_ref = fmaxf(mx, __shfl_xor(mx, 32, 64));  // the reference: the first tile's maximum
+      m_seen = fmaxf(m_seen, mx);
+      const bool over = mx > m_ref + kSlack;
+      float p[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], sl2, -m_ref));
+      float ls = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; v += 4) ls += (p[v] + p[v + 1]) + (p[v + 2] + p[v + 3]);
+      l_run += ls;
+      uint4 c0, c1;
+      c0.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[0], p[1]}, bf16x2));
+      c0.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[2], p[3]}, bf16x2));
+      c0.z = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[4], p[5]}, bf16x2));
+      c0.w = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[6], p[7]}, bf16x2));
+      c1.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[8], p[9]}, bf16x2));
+      c1.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[10], p[11]}, bf16x2));
+      c1.z = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[12], p[13]}, bf16x2));
+      c1.w = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[14], p[15]}, bf16x2));
+      unsigned char *pt = sP[tile & 1];
+      *reinterpret_cast<uint4 *>(pt + pw0) = c0;
+      *reinterpret_cast<uint4 *>(pt + pw1) = c1;
+      const bool anyo = __any(over);
+      if (lane == 0) sFlag[tile & 1][hh] = anyo ? 1 : 0;
+    };
+
+    for (int attempt = 0;; ++attempt) {
+      l_run = 0.f;
+      lds_barrier();  // pointer tables of the first tiles copied
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers
+      lds_barrier();  // tile 0 landed
+      bool restart = false;
+      for (int it = -1; it < T; ++it) {
+        if (it >= 0 && overflowed(it) && attempt < kMaxRestarts) {
+          restart = true;
+          break;
+        }
+        if (it + 1 < T) process(it + 1, qk_tile(it + 1), it + 1 == 0 && attempt == 0);
+        if (it == T - 1) break;
+        lds_barrier();
+      }
+      if (!restart) break;
+      lds_barrier();  // every wave has left the loop, copies drained
+      m_ref = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));  // restart from the largest logit seen
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    return f32x4{s0[0] + s1[0], s0[1] + s1[1], s0[2] + s1[2], s0[3] + s1[3]};
-  };
-  // Lane holds keys 16 kh + 4 g4 + 0..3 of head `head`; keys past the split are -inf.
-  auto masked = [&](int it, f32x4 s) {
-    const int nvalid = nkeys - it * kKT;
-    float sv[4] = {s[0], s[1], s[2], s[3]};
-    if (nvalid < kKT) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (16 * kh + 4 * g4 + r >= nvalid) sv[r] = -INFINITY;
-    }
-    return f32x4{sv[0], sv[1], sv[2], sv[3]};
-  };
-  // Probabilities against the reference, published as bf16 P^T with the
-  // overflow flag of this wave.
-  auto softmax_tile = [&](int it, f32x4 sv) {
-    const float mloc = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])) * sl2;
-    m_seen = fmaxf(m_seen, mloc);
-    const bool over = mloc > m_ref + kSlack;
-    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[0], sl2, -m_ref));
-    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[1], sl2, -m_ref));
-    const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[2], sl2, -m_ref));
-    const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[3], sl2, -m_ref));
-    l_run += (p0 + p1) + (p2 + p3);
-    uint2 pq;
-    pq.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
-    pq.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p2, p3}, bf16x2));
-    *reinterpret_cast<uint2 *>(&sP[it & 1][pw]) = pq;
-    const bool anyo = __any(over);
-    if (lane == 0) sFlag[it & 1][wv] = anyo ? 1 : 0;
-  };
-  // O^T += V^T P^T for tile `it`, this wave's value channels, both head tiles.
-  auto pv_tile = [&](int it) {
-    const unsigned char *kt = sK[it % kNBUF];
-    const unsigned char *pt = sP[it & 1];
-#pragma unroll
-    for (int ks = 0; ks < kKT / 16; ++ks) {
-      bf16x8 pb[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) pb[t] = *reinterpret_cast<const bf16x8 *>(pt + p_off(32 * t + l32, 2 * ks + hi));
-#pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
-        const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks + 1][ct]));
-        const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
-                                                         v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[t], acc_o[t][ct], 0, 0, 0);
+    // Row sums per head: the two lanes of a head (fixed order).
+    const float lsum = l_run + __shfl_xor(l_run, 32, 64);
+    lds_barrier();
+    if (hi == 0) {
+      sSum[head] = lsum;
+      sRef[head] = m_ref;
+      if (single) {
+        if (lse) lse[node * kH + head] = (m_ref + __log2f(lsum)) * kLn2;
+      } else {
+        part_ml[(((node * splits) + split) * kH + head) * 2 + 0] = m_ref;
+        part_ml[(((node * splits) + split) * kH + head) * 2 + 1] = lsum;
       }
     }
-  };
-  // the largest of v over the lanes holding this lane's head (same l16), then
-  // over the two key halves through LDS; every lane gets its head's value
-  auto head_max = [&](float v) {
-    v = fmaxf(v, __shfl_xor(v, 16, 64));
-    v = fmaxf(v, __shfl_xor(v, 32, 64));
-    if (g4 == 0) sMx[kh][head] = v;
     lds_barrier();
-    return fmaxf(sMx[0][head], sMx[1][head]);
-  };
-
-  for (int attempt = 0;; ++attempt) {
+  } else if (wv == 4 || wv == 5) {
+    // ---- copy wave: column groups [g_lo, g_hi) of every tile -------------------
+    const int pr = wv - 4;
+    const int g_lo = pr ? kG0 : 0, g_hi = pr ? kGroups : kG0;
+    const int n_g = 4 * (g_hi - g_lo);
+    const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+    const uint32_t lds_k = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
+    const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
+    // Pointer table of tile u: lane l copies 4 bytes (half l & 1) of the
+    // pointer of key min(32 u + l / 2, nkeys - 1), so rows past the split's
+    // end repeat its last key (finite data; their probabilities are 0).
+    auto copy_ptrs = [&](int u) {
+      const int r = std::min(u * kKT + (lane >> 1), nkeys - 1);
+      dma4(reinterpret_cast<const unsigned char *>(tab + r) + 4 * (lane & 1), lds_p + (u % kPSlots) * (kKT * 8));
+    };
+    // Rows of tile u into buffer u % 4: instruction (g, k) fills rows
+    // 8k .. 8k+7 of group g (lane = row-in-8 * 8 + slot); slot s of row r
+    // holds logical chunk slot(r, s) of the group.
+    auto copy_tile = [&](int u) {
+      const unsigned char *src[4];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int ct = 0; ct < 2; ++ct) acc_o[t][ct] = f32x16{};
-    l_run = 0.f;
-    bool restart = false;
-    // tiles 0, 1, 2 into buffers 0, 1, 2; wait for tile 0
-    load_srcs(0);
-    issue_tile(0);
-    if (ntiles > 1) {
-      load_srcs(1);
-      issue_tile(1);
-    }
-    if (ntiles > 2) {
-      load_srcs(2);
-      issue_tile(2);
-      vm_wait<2 * kNPW>();
-    } else if (ntiles > 1) {
-      vm_wait<kNPW>();
-    } else {
-      vm_wait<0>();
-    }
-    __syncthreads();
-    const f32x4 s_first = masked(0, qk_tile(0));
-    if (attempt == 0)  // the reference: the first tile's maximum per head
-      m_ref = head_max(fmaxf(fmaxf(s_first[0], s_first[1]), fmaxf(s_first[2], s_first[3])) * sl2);
-    softmax_tile(0, s_first);
-    if (ntiles > 2)
-      vm_wait<kNPW>();
-    else
-      vm_wait<0>();
-    lds_barrier();
-
-    for (int it = 0; it < ntiles; ++it) {
-      const bool more = it + 1 < ntiles;
-      int anyf = 0;  // overflow flags of the probabilities of tile it
-#pragma unroll
-      for (int w = 0; w < kNW; ++w) anyf |= sFlag[it & 1][w];
-      if (it + 3 < ntiles) load_srcs(it + 3);
-      if (more) softmax_tile(it + 1, masked(it + 1, qk_tile(it + 1)));
-      pv_tile(it);
-      if (anyf) {  // probabilities of tile it overflowed the reference
-        restart = attempt < kMaxRestarts;
-        if (restart) break;
+      for (int k = 0; k < 4; ++k) {
+        const int r = 8 * k + (lane >> 3);
+        src[k] = reinterpret_cast<const unsigned char *>(sPtr[u % kPSlots][r]) + slot(r, lane & 7) * 16;
       }
-      if (it + 3 < ntiles) issue_tile(it % kNBUF);  // this wave's reads of buffer it % 3 are done
-      if (!more) break;
-      // this wave's copies of tile it+2 have landed (those of tile it+3 may still fly)
-      if (it + 3 < ntiles)
-        vm_wait<kNPW>();
-      else
+      const uint32_t dst = lds_k + (u % kNBUF) * kTB;
+      for (int g = g_lo; g < g_hi; ++g)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dma16(src[k] + g * 128, dst + g * kGB + k * 1024);
+    };
+
+    for (int attempt = 0;; ++attempt) {
+      if (pr == 0) {
+        for (int u = 0; u < std::min(T, 5); ++u) copy_ptrs(u);
         vm_wait<0>();
+      }
+      lds_barrier();  // pointer tables of tiles 0..4 copied
+      copy_tile(0);
+      if (T > 1) copy_tile(1);
+      vm_wait_n(T > 1 ? n_g : 0);
+      lds_barrier();  // tile 0 landed
+      bool restart = false;
+      for (int it = -1; it < T; ++it) {
+        if (it >= 0 && overflowed(it) && attempt < kMaxRestarts) {
+          restart = true;
+          break;
+        }
+        int n = 0;
+        if (pr == 0 && it + 6 < T) {
+          copy_ptrs(it + 6);
+          n += 1;
+        }
+        if (it + 3 < T) {
+          copy_tile(it + 3);  // buffer (it+3) % 4 held tile it-1, read before the last barrier
+          n += n_g;
+        }
+        if (it == T - 1) break;
+        vm_wait_n(n);  // tile it+2 has landed (tile it+3 and the pointer table may still fly)
+        lds_barrier();
+      }
+      if (!restart) break;
+      vm_wait<0>();
       lds_barrier();
     }
-    if (!restart) break;
-    // restart from the largest logit any lane has seen, per head
-    vm_wait<0>();
-    __syncthreads();
-    m_ref = head_max(m_seen);
-    __syncthreads();
-  }
-
-  // Row sums per head: the four lanes of a head in a wave (fixed order), then
-  // the two key halves; references per head.
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  __syncthreads();
-  if (g4 == 0) {
-    sMx[kh][head] = l_run;
-    if (kh == 0) sRef[head] = m_ref;
-  }
-  __syncthreads();
-  float lsum[2], mref[2];
+    lds_barrier();
+    lds_barrier();
+  } else {
+    // ---- value wave: channels 128 pq .. 128 pq + 127 for all heads -------------
+    const int pq = (wv & 1) | ((wv >> 2) << 1);
+    const int g = lane >> 4, jj = lane & 15;
+    // Transpose-read offsets: rows 16 ks + 8 s + 4 hi + jj/4, columns
+    // 128 pq + 32 ct + 16 (g & 1) + 4 (jj & 3).
+    int voff[4][4];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    lsum[t] = sMx[0][32 * t + l32] + sMx[1][32 * t + l32];
-    mref[t] = sRef[32 * t + l32];
-  }
-
-  // epilogue: lane holds, per head tile t, head 32t + l32 and value rows
-  // 64wv + 32ct + 8(j/4) + 4hi + (j%4)
-  const bool single = n_keys <= chunk;
+    for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int h = t * 32 + l32;
-    const float inv = single ? 1.0f / lsum[t] : 1.0f;
+      for (int ct = 0; ct < 4; ++ct)
+        voff[rr][ct] = off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
+                           128 * pq + 32 * ct + 16 * (g & 1) + 4 * (jj & 3));
+    f32x16 acc_o[2][4];
+    auto pv_tile = [&](int it) {
+      const unsigned char *kt = sK[it % kNBUF];
+      const unsigned char *pt = sP[it & 1];
+      bf16x8 pb[2][2];
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct)
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int col = wv * 64 + 32 * ct + 8 * jq + 4 * hi;
-        const float v0 = acc_o[t][ct][4 * jq] * inv, v1 = acc_o[t][ct][4 * jq + 1] * inv;
-        const float v2 = acc_o[t][ct][4 * jq + 2] * inv, v3 = acc_o[t][ct][4 * jq + 3] * inv;
-        if (single) {
-          uint2 w;
-          w.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v0, v1}, bf16x2));
-          w.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v2, v3}, bf16x2));
-          *reinterpret_cast<uint2 *>(out + (node * kH + h) * kDV + col) = w;
-        } else {
-          *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * kH + h) * kDV + col) =
-              make_float4(v0, v1, v2, v3);
+        for (int t = 0; t < 2; ++t) pb[ks][t] = *reinterpret_cast<const bf16x8 *>(pt + p_off(32 * t + l32, 2 * ks + hi));
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+          const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
+          const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks + 1][ct]));
+          const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+                                                           v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+            acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks][t], acc_o[t][ct], 0, 0, 0);
         }
+    };
+
+    for (int attempt = 0;; ++attempt) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) acc_o[t][ct] = f32x16{};
+      lds_barrier();
+      lds_barrier();
+      bool restart = false;
+      for (int it = -1; it < T; ++it) {
+        if (it >= 0) {
+          if (overflowed(it) && attempt < kMaxRestarts) {
+            restart = true;
+            break;
+          }
+          pv_tile(it);
+        }
+        if (it == T - 1) break;
+        lds_barrier();
       }
-    if (wv == 0 && hi == 0) {
-      if (single) {
-        if (lse) lse[node * kH + h] = (mref[t] + __log2f(lsum[t])) * kLn2;
-      } else {
-        part_ml[(((node * splits) + split) * kH + h) * 2 + 0] = mref[t];
-        part_ml[(((node * splits) + split) * kH + h) * 2 + 1] = lsum[t];
-      }
+      if (!restart) break;
+      lds_barrier();
+    }
+    lds_barrier();
+    lds_barrier();  // sums and references published
+    // Epilogue: lane holds, per head tile t, head 32 t + l32 and value
+    // channels 128 pq + 32 ct + 8 (j / 4) + 4 hi + (j % 4).
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int h = t * 32 + l32;
+      const float inv = single ? 1.0f / sSum[h] : 1.0f;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq) {
+          const int col = 128 * pq + 32 * ct + 8 * jq + 4 * hi;
+          const float v0 = acc_o[t][ct][4 * jq] * inv, v1 = acc_o[t][ct][4 * jq + 1] * inv;
+          const float v2 = acc_o[t][ct][4 * jq + 2] * inv, v3 = acc_o[t][ct][4 * jq + 3] * inv;
+          if (single) {
+            uint2 w;
+            w.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v0, v1}, bf16x2));
+            w.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v2, v3}, bf16x2));
+            *reinterpret_cast<uint2 *>(out + (node * kH + h) * kDV + col) = w;
+          } else {
+            *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * kH + h) * kDV + col) =
+                make_float4(v0, v1, v2, v3);
+          }
+        }
     }
   }
 }
