@@ -34,7 +34,7 @@ static tv_status check_dims(const tv_dims *dp) {
   if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window, d.ratio_csa, d.ratio_hca})) return TV_ERR_INVALID_ARG;
   if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
   if (!std::isfinite(d.scale) || !(d.scale > 0.f)) return TV_ERR_INVALID_ARG;
-  if (d.B > 4096 || !shape_supported(d)) return TV_ERR_UNSUPPORTED;
+  if (d.B > 4096 || !shape_supported(d) || !topk_supported(d)) return TV_ERR_UNSUPPORTED;
   return TV_OK;
 }
 
@@ -109,6 +109,14 @@ WsLayout ws_layout(const tv_dims &d) {
   off = align256(off + sizeof(void *) * nodes * w.plan.max_keys);
   w.nkeys = off;
   off = align256(off + sizeof(int32_t) * nodes);
+  const int tseg = topk_max_segments(d);
+  const int64_t surv = tseg > 1 ? nodes * tseg * d.topk : 0;
+  w.surv_idx = off;
+  off = align256(off + sizeof(int32_t) * surv);
+  w.surv_key = off;
+  off = align256(off + sizeof(uint32_t) * surv);
+  w.surv_cnt = off;
+  off = align256(off + sizeof(int32_t) * (tseg > 1 ? nodes * tseg : 0));
   w.total = off;
   return w;
 }
@@ -242,9 +250,15 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
   int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
   const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
   int32_t *nkeys = reinterpret_cast<int32_t *>(ws + w.nkeys);
+  int32_t *surv_idx = reinterpret_cast<int32_t *>(ws + w.surv_idx);
+  uint32_t *surv_key = reinterpret_cast<uint32_t *>(ws + w.surv_key);
+  int32_t *surv_cnt = reinterpret_cast<int32_t *>(ws + w.surv_cnt);
   TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
                                        w.score_stride, selp, row_status, row_order, keytab, w.plan.max_keys, nkeys,
-                                       stream));
+                                       surv_idx, surv_key, surv_cnt, stream));
+  if (topk_max_segments(d) > 1)
+    TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, keytab, w.plan.max_keys,
+                                              surv_idx, surv_key, surv_cnt, stream));
   TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys, w.plan, part_o, part_ml, out, lse,
                                        stream));
   if (w.plan.splits > 1)

@@ -21,38 +21,61 @@ struct NodeKeys {
   int64_t p, win_lo;
 };
 
-// Fills path[d] (ancestor at depth d, d <= depth of i) and hca_node[t] (t-th
-// path node closing an HCA block) in shared memory; must be called by every
-// thread of the block (contains barriers).
-__device__ inline NodeKeys node_keys(const tv_dims &d, int32_t L, int b, int i, const uint64_t *anc,
-                                     const int32_t *depth, int32_t *path, int32_t *hca_node, int32_t *cnt) {
-  const int tid = threadIdx.x;
-  const uint64_t m = anc[(int64_t)b * d.D + i];
-  if (tid == 0) { cnt[0] = 0; cnt[1] = 0; }
-  __syncthreads();
-  if (tid < d.D && ((m >> tid) & 1ull)) {
-    const int dj = depth[(int64_t)b * d.D + tid];
-    path[dj] = tid;
-    const int64_t pj = (int64_t)L + dj;
-    if ((pj + 1) % d.ratio_csa == 0) atomicAdd(&cnt[0], 1);
-    if ((pj + 1) % d.ratio_hca == 0) hca_node[(pj + 1) / d.ratio_hca - 1 - L / d.ratio_hca] = tid;
-    if ((pj + 1) % d.ratio_hca == 0) atomicAdd(&cnt[1], 1);
-  }
-  __syncthreads();
+// Key counts of a node at depth di whose root path closes ncsa CSA and nhca
+// HCA blocks.
+__device__ inline NodeKeys make_node_keys(const tv_dims &d, int32_t L, int di, int ncsa, int nhca) {
   NodeKeys k;
   k.L = L;
-  k.p = (int64_t)L + depth[(int64_t)b * d.D + i];
+  k.p = (int64_t)L + di;
   k.n4 = L / d.ratio_csa;
   k.n128 = L / d.ratio_hca;
-  const int cand = k.n4 + cnt[0];
+  const int cand = k.n4 + ncsa;
   k.nsel = cand < d.topk ? cand : d.topk;
-  k.s128 = cnt[1];
+  k.s128 = nhca;
   const int64_t lo = k.p - d.window + 1;
   k.win_lo = lo > 0 ? lo : 0;
   k.nwin_c = (int32_t)(k.win_lo < L ? L - k.win_lo : 0);
   const int64_t pstart = k.win_lo > L ? k.win_lo : L;
   k.npath = (int32_t)(k.p - pstart + 1);
   k.n_keys = k.nsel + k.n128 + k.s128 + k.nwin_c + k.npath;
+  return k;
+}
+
+// Root-path structure of node i of row b, computed by every wavefront from
+// the ancestor mask m and dl, the depth of the row's node `lane` (lanes below
+// D): path[d] (ancestor at depth d) and hca_node[t] (t-th path node closing an
+// HCA block) are written to shared memory by wavefront 0 and are visible
+// after the caller's next barrier; the returned counts need no barrier.
+// csa_mask gets the path nodes closing a CSA block (bit = node index; on one
+// root path node index order is depth order).
+__device__ inline NodeKeys path_keys(const tv_dims &d, int32_t L, int i, uint64_t m, int dl, int32_t *path,
+                                     int32_t *hca_node, uint64_t &csa_mask) {
+  const int lane = threadIdx.x & 63;
+  const bool onp = lane < d.D && ((m >> lane) & 1ull);
+  const int32_t pl = L + dl;  // positions stay below 2^30
+  const bool c4c = onp && (pl + 1) % d.ratio_csa == 0;
+  const bool hcc = onp && (pl + 1) % d.ratio_hca == 0;
+  csa_mask = __ballot(c4c);
+  const uint64_t hca_mask = __ballot(hcc);
+  if ((threadIdx.x >> 6) == 0) {
+    if (onp) path[dl] = lane;
+    if (hcc) hca_node[(pl + 1) / d.ratio_hca - 1 - L / d.ratio_hca] = lane;
+  }
+  return make_node_keys(d, L, __shfl(dl, i, 64), __popcll(csa_mask), __popcll(hca_mask));
+}
+
+// Fills path[d] (ancestor at depth d, d <= depth of i) and hca_node[t] (t-th
+// path node closing an HCA block) in shared memory; must be called by every
+// thread of the block (contains barriers).
+__device__ inline NodeKeys node_keys(const tv_dims &d, int32_t L, int b, int i, const uint64_t *anc,
+                                     const int32_t *depth, int32_t *path, int32_t *hca_node, int32_t *cnt) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t m = anc[(int64_t)b * d.D + i];
+  const int dl = lane < d.D ? depth[(int64_t)b * d.D + lane] : 0;
+  uint64_t csa_mask;
+  const NodeKeys k = path_keys(d, L, i, m, dl, path, hca_node, csa_mask);
+  (void)cnt;
+  __syncthreads();
   return k;
 }
 

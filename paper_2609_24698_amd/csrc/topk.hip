@@ -6,17 +6,23 @@
 // scratch indexer keys): a node never sees an entry compressed on another
 // branch (Sec. 3.1, Sec. 4.1).
 //
-// Selection is an exact radix select on order-preserving 32-bit keys: digits
-// of at most 8 bits, starting below the bits that all keys share, counted in
-// an LDS histogram kept in eight interleaved copies so that equal digits in
-// one wavefront collide at most eight ways.  An ordered compaction then lists
-// the keys above the threshold and the lowest-index keys equal to it.  When a
-// node's candidates fit, the keys live in LDS; otherwise every pass re-reads
-// the global scores.
+// Selection is an exact radix select on order-preserving 32-bit keys held in
+// registers (element e of a workgroup in slot e / 512 of thread e % 512):
+// 13-bit digits counted in an LDS histogram, each pass restricted to the keys
+// that share the digits found so far, until the bin holding the topk-th key
+// holds exactly the keys still needed or every bit is fixed.  An ordered
+// compaction then lists the keys above the threshold and the lowest-index
+// keys equal to it, from the registers.
 //
-// Each workgroup finally writes its node's key list (one latent-row pointer
-// per key, in attention order) so that the attention kernel starts from a
-// table instead of re-deriving it.
+// A node with up to kTopkSeg committed entries is selected by one workgroup.
+// A longer node is cut into segments of kTopkSeg entries: each segment's
+// workgroup keeps its own topk (a superset of its share of the node's topk),
+// and a merge kernel selects the node's topk among the survivors of all its
+// segments, which are already in index order.
+//
+// The selecting workgroup also writes its node's key list (one latent-row
+// pointer per key, in attention order) so that the attention kernel starts
+// from a table instead of re-deriving it.
 #include <algorithm>
 
 #include "node_keys.h"
@@ -26,11 +32,22 @@
 namespace tv {
 
 constexpr int kMaxScratch = 64;
-constexpr int kLdsKeys = 16384 + 256;  // candidates held in LDS (65 KiB): rows up to L = 65536 plus a path
-constexpr int kNT = 512;               // threads per workgroup
-constexpr int kNW = kNT / 64;
-constexpr int kCopies = 8;             // interleaved histogram copies
-static_assert(kLdsKeys % 4 == 0, "LDS keys are staged as 16-byte groups");
+constexpr int kTkNT = 512;  // threads of a selecting workgroup
+constexpr int kTkNW = kTkNT / 64;
+constexpr int kTkKPT = 34;  // keys per thread of a segment: kTopkSeg committed entries plus up to 64 path entries
+constexpr int kTkBits = 13, kTkBins = 1 << kTkBits;
+static_assert(kTkNT * kTkKPT >= kTopkSeg + kMaxScratch, "segment plus path entries fit the registers");
+static_assert(kTkNT * kTopkMergeKPT == kTopkMergeCap, "merge capacity");
+
+struct __align__(16) SelShared {
+  uint32_t hist[kTkBins];
+  int wsum[kTkNW];
+  int found[3];
+  int cnt[2][kTopkMergeKPT][kTkNW];  // per slot and wave: keys above the threshold, keys equal to it
+};
+
+// Barrier for shared-memory hand-offs only: global loads in flight stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b) {
   float s = bf2f_lo(a.x) * bf2f_lo(b.x);
@@ -44,92 +61,287 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b) {
   return s;
 }
 
-template <bool kLds>
-__global__ void __launch_bounds__(kNT) topk_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
-                                                   const uint64_t *__restrict__ anc,
-                                                   const int32_t *__restrict__ depth,
-                                                   const uint16_t *__restrict__ scr_c4,
-                                                   const uint16_t *__restrict__ scr_c128,
-                                                   const uint16_t *__restrict__ q_idx,
-                                                   const uint16_t *__restrict__ w_idx,
-                                                   const float *__restrict__ scores, int score_stride,
-                                                   int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
-                                                   int32_t *__restrict__ row_order,
-                                                   const uint16_t **__restrict__ keytab, int keytab_stride,
-                                                   int32_t *__restrict__ nkeys_tab) {
-  __shared__ __align__(16) uint32_t keys[kLds ? kLdsKeys : 4];
-  __shared__ __align__(16) uint32_t hist[256 * kCopies];
-  __shared__ float scr_score[kMaxScratch];
-  __shared__ int32_t scr_node[kMaxScratch];
-  __shared__ uint32_t mm[2][kNW];
-  __shared__ int wcnt[2][kNW];
-  __shared__ uint32_t found[3];
-  __shared__ int32_t path[64], hca_node[64], cnt[2];
+// Threshold of the k largest of the keys the workgroup holds (key[j] is
+// element tid + 512 j; elements from n on, and any other padding, hold key 0,
+// below every real key, and are never counted or taken; k < the number of
+// real keys).  On return
+// every thread has prefix, pmask and remaining such that the k largest are the
+// keys with (key & pmask) > prefix and the `remaining` lowest elements with
+// (key & pmask) == prefix.
+template <int KPT>
+__device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int n, int k, SelShared &sh,
+                                                uint32_t &prefix, uint32_t &pmask, int &remaining) {
+  const int nr = (n + kTkNT - 1) / kTkNT;  // slots that hold any element below n
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int b = blockIdx.x / d.D;
-  const int i = blockIdx.x - b * d.D;
-  if (i == 0) {
+  prefix = 0;
+  pmask = 0;
+  remaining = k;
+  for (int shift = 32; shift > 0;) {
+    const int nb = shift < kTkBits ? shift : kTkBits;
+    const int sft = shift - nb;
+    const int nbins = 1 << nb;
+    const uint32_t dmask = (uint32_t)nbins - 1u;
+    for (int t = tid; t < nbins / 4; t += kTkNT) reinterpret_cast<uint4 *>(sh.hist)[t] = make_uint4(0, 0, 0, 0);
+    lds_barrier();
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+      if (j < nr && key[j] != 0u && (key[j] & pmask) == prefix) atomicAdd(&sh.hist[(key[j] >> sft) & dmask], 1u);
+    lds_barrier();
+    // Thread t owns the 16 bins from nbins - 16 (t + 1) up (threads 0.. hold
+    // the top bins), read as four 16-byte groups; counts scan from the top.
+    const int hb = nbins - 16 * (tid + 1);
+    uint32_t h[16];
+    if (hb >= 0) {
+      const uint4 *g4 = reinterpret_cast<const uint4 *>(sh.hist + hb);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint4 x = g4[u];
+        h[4 * u] = x.x;
+        h[4 * u + 1] = x.y;
+        h[4 * u + 2] = x.z;
+        h[4 * u + 3] = x.w;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) h[u] = 0u;
+    }
+    int local = 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) local += (int)h[u];
+    int incl = local;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) sh.wsum[wv] = incl;
+    lds_barrier();
+    int above = incl - local;
+#pragma unroll
+    for (int w = 0; w < kTkNW; ++w) above += w < wv ? sh.wsum[w] : 0;
+    if (above < remaining && remaining <= above + local) {
+#pragma unroll
+      for (int u = 15; u >= 0; --u) {
+        const int c = (int)h[u];
+        if (above < remaining && remaining <= above + c) {
+          sh.found[0] = hb + u;
+          sh.found[1] = above;
+          sh.found[2] = c;
+        }
+        above += c;
+      }
+    }
+    lds_barrier();
+    prefix |= (uint32_t)sh.found[0] << sft;
+    pmask |= dmask << sft;
+    remaining -= sh.found[1];
+    const int c = sh.found[2];
+    shift = sft;
+    if (c == remaining) break;  // every key of the bin is taken
+  }
+}
+
+// Ordered compaction of the keys the threshold takes: the element index of
+// the pos-th taken key (in element order) goes to list[pos], pos < k.  The
+// list aliases the histogram, which the threshold search no longer needs.
+template <int KPT>
+__device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n, uint32_t prefix, uint32_t pmask,
+                                              int remaining, SelShared &sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int nr = (n + kTkNT - 1) / kTkNT;
+  // lane j % 64 keeps this wave's counts of slot j (in set j / 64)
+  constexpr int kSets = (KPT + 63) / 64;
+  int my_g[kSets] = {}, my_q[kSets] = {};
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    if (j < nr) {
+      const uint32_t km = key[j] & pmask;
+      const int g = __popcll(__ballot(km > prefix));
+      const int q = __popcll(__ballot(km == prefix && key[j] != 0u));
+      my_g[j >> 6] = lane == (j & 63) ? g : my_g[j >> 6];
+      my_q[j >> 6] = lane == (j & 63) ? q : my_q[j >> 6];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kSets; ++u)
+    if (64 * u + lane < KPT) {
+      sh.cnt[0][64 * u + lane][wv] = my_g[u];
+      sh.cnt[1][64 * u + lane][wv] = my_q[u];
+    }
+  lds_barrier();
+  // exclusive prefix over (slot, wave) in element order, by wave 0
+  if (wv == 0) {
+    constexpr int kE = KPT * kTkNW;
+    constexpr int kPer = (kE + 63) / 64;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      int *base = &sh.cnt[a][0][0];
+      int v[kPer], loc = 0;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int x = lane * kPer + u;
+        v[u] = x < kE ? base[x] : 0;
+        loc += v[u];
+      }
+      int incl = loc;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      int run = incl - loc;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int x = lane * kPer + u;
+        if (x < kE) base[x] = run;
+        run += v[u];
+      }
+    }
+  }
+  lds_barrier();
+  // lane j % 64 holds this wave's offsets of slot j; slot j reads them from lane j
+#pragma unroll
+  for (int u = 0; u < kSets; ++u) {
+    my_g[u] = 64 * u + lane < KPT ? sh.cnt[0][64 * u + lane][wv] : 0;
+    my_q[u] = 64 * u + lane < KPT ? sh.cnt[1][64 * u + lane][wv] : 0;
+  }
+  int32_t *list = reinterpret_cast<int32_t *>(sh.hist);
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    if (j < nr) {
+      const uint32_t km = key[j] & pmask;
+      const bool gt = km > prefix, eq = km == prefix && key[j] != 0u;
+      const uint64_t bg = __ballot(gt), be = __ballot(eq);
+      const int g = __builtin_amdgcn_readlane(my_g[j >> 6], j & 63) +
+                    (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bg >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bg, 0u));
+      const int q = __builtin_amdgcn_readlane(my_q[j >> 6], j & 63) +
+                    (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(be >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)be, 0u));
+      const int pos = gt ? g + std::min(q, remaining) : g + q;
+      if (gt || (eq && q < remaining)) list[pos] = tid + kTkNT * j;
+    }
+  }
+  lds_barrier();
+}
+
+// Latent row of CSA entry s of node (b, i): committed entries from the pool,
+// path entries from the scratch slot of the path node that closed them.
+__device__ __forceinline__ const uint16_t *csa_row(const tv_dims &d, const NodeKeys &nk, int b, int s,
+                                                   const int32_t *path, const uint16_t *c4, int64_t c4b,
+                                                   const uint16_t *scr_c4) {
+  if (s < nk.n4) return c4 + (c4b + s) * d.d_row;
+  int64_t dd = (int64_t)(s + 1) * d.ratio_csa - 1 - nk.L;
+  if (dd < 0 || dd > nk.p - nk.L) dd = 0;  // defensive: stay on the node's own path
+  return scr_c4 + ((int64_t)b * d.D + path[dd]) * (d.d_row + d.d_idx);
+}
+
+// Key of a real candidate: the order-preserving key, at least 1, so that the
+// padding key 0 sorts below every candidate (only the two all-ones negative
+// NaN patterns share key 1).
+__device__ __forceinline__ uint32_t live_key(float s) { return max(score_key(s), 1u); }
+
+__device__ __forceinline__ int topk_segments(int n4) { return n4 <= kTopkSeg ? 1 : (n4 + kTopkSeg - 1) / kTopkSeg; }
+
+// One workgroup per (node, segment).  Segment 0 of node 0 of a row also ranks
+// the row by length for the attention's row order, and segment 0 of every
+// node writes the node's non-CSA keys into its key table.
+__global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4))) topk_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
+                                                     const uint64_t *__restrict__ anc,
+                                                     const int32_t *__restrict__ depth,
+                                                     const uint16_t *__restrict__ scr_c4,
+                                                     const uint16_t *__restrict__ scr_c128,
+                                                     const uint16_t *__restrict__ q_idx,
+                                                     const uint16_t *__restrict__ w_idx,
+                                                     const float *__restrict__ scores, int score_stride,
+                                                     int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
+                                                     int32_t *__restrict__ row_order,
+                                                     const uint16_t **__restrict__ keytab, int keytab_stride,
+                                                     int32_t *__restrict__ nkeys_tab, int max_seg,
+                                                     int32_t *__restrict__ surv_idx, uint32_t *__restrict__ surv_key,
+                                                     int32_t *__restrict__ surv_cnt) {
+  __shared__ SelShared sh;
+  __shared__ float scr_score[kMaxScratch];
+  __shared__ int wcnt[kTkNW];
+  __shared__ int32_t path[64], hca_node[64];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t node = blockIdx.x / max_seg;
+  const int seg = blockIdx.x - (int)node * max_seg;
+  const int b = (int)(node / d.D);
+  const int i = (int)(node - (int64_t)b * d.D);
+  // one round trip: everything whose address is known from (row, node, lane)
+  const int32_t status = row_status[b];
+  const int32_t L = c.len[b];
+  const uint64_t m = anc[node];
+  const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
+  const int dl = lane < d.D ? depth[(int64_t)b * d.D + lane] : 0;  // depth of the row's node `lane`
+  const int hl = lane >> 3, cc = lane & 7;  // path-entry scoring: head h0 + hl, channels 8cc..8cc+7
+  uint4 qv0 = make_uint4(0, 0, 0, 0);
+  float wh0 = 0.f;
+  if (hl < d.H_idx) {
+    qv0 = *reinterpret_cast<const uint4 *>(q_idx + (node * d.H_idx + hl) * 64 + 8 * cc);
+    wh0 = bf2f(w_idx[node * d.H_idx + hl]);
+  }
+  if (i == 0 && seg == 0) {
     // Rank of row b by (committed length descending, row ascending), for every
-    // row whatever its status: row_order[rank] = b.  The attention kernel
-    // starts the longest rows first.
-    const int32_t Lb = c.len[b];
-    int cnt = 0;
-    for (int r = tid; r < d.B; r += kNT) {
+    // row whatever its status: row_order[rank] = b.
+    int nb = 0;
+    for (int r = tid; r < d.B; r += kTkNT) {
       const int32_t Lr = c.len[r];
-      cnt += (Lr > Lb || (Lr == Lb && r < b)) ? 1 : 0;
+      nb += (Lr > L || (Lr == L && r < b)) ? 1 : 0;
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-    if (lane == 0) wcnt[1][wv] = cnt;
+    for (int o = 32; o > 0; o >>= 1) nb += __shfl_xor(nb, o, 64);
+    if (lane == 0) wcnt[wv] = nb;
     __syncthreads();
     if (tid == 0) {
       int rank = 0;
-      for (int w = 0; w < kNW; ++w) rank += wcnt[1][w];
+      for (int w = 0; w < kTkNW; ++w) rank += wcnt[w];
       row_order[rank] = b;
     }
   }
-  if (row_status[b] != TV_ROW_OK) return;
-  const int32_t L = c.len[b];
+  if (status != TV_ROW_OK) return;
   if (!len_ok(L, d.max_len)) {
-    if (i == 0 && tid == 0) row_status[b] = TV_ROW_BAD_LEN;
+    if (i == 0 && seg == 0 && tid == 0) row_status[b] = TV_ROW_BAD_LEN;
     return;
   }
-  const int64_t node = (int64_t)b * d.D + i;
   const int n4 = L / d.ratio_csa;
-  const uint64_t m = anc[node];
+  const int nseg = topk_segments(n4);
+  if (seg >= nseg) return;
+  const bool last = seg == nseg - 1;
+  const int c0 = seg * kTopkSeg;
+  const int cn = std::min(n4, c0 + kTopkSeg) - c0;  // committed candidates of this segment
+  const float *sc = scores + node * score_stride + c0;
+  // committed scores in flight while the path entries are scored (loads of
+  // slots past the segment re-read its last entry, or entry 0 of the row)
+  uint32_t key[kTkKPT];  // score bits first, converted to keys below
+#pragma unroll
+  for (int j = 0; j < kTkKPT; ++j)
+    key[j] = __float_as_uint(sc[std::max(std::min(tid + kTkNT * j, cn - 1), 0)]);
   const int d_u = d.d_row + d.d_idx;
 
+  // The node's root path (its key layout) from the ancestor mask, no barrier.
+  uint64_t csa_mask;
+  const NodeKeys nk = path_keys(d, L, i, m, dl, path, hca_node, csa_mask);
+
   // Entries closed on the root path take the consecutive logical indices
-  // n4, n4+1, ... in depth order.
-  bool closes = false;
-  if (tid < d.D && ((m >> tid) & 1ull)) {
-    const int64_t p = (int64_t)L + depth[(int64_t)b * d.D + tid];
-    if ((p + 1) % d.ratio_csa == 0) {
-      closes = true;
-      scr_node[(p + 1) / d.ratio_csa - 1 - n4] = tid;
-    }
-  }
-  if (wv == 0) {
-    const int cnt = __popcll(__ballot(closes));
-    if (lane == 0) wcnt[0][0] = cnt;
-  }
-  __syncthreads();
-  const int nscr = wcnt[0][0];
-  // Scores of the path entries.  Wave w takes entries w, w + 8, ...; lane
-  // (h8, c) holds channels 8c..8c+7 of head h0 + h8, for head groups h0.
-  {
-    const int hl = lane >> 3, cc = lane & 7;
-    for (int t = wv; t < nscr; t += kNW) {
-      const uint4 kv = *reinterpret_cast<const uint4 *>(scr_c4 + ((int64_t)b * d.D + scr_node[t]) * d_u + d.d_row +
-                                                        8 * cc);
+  // n4, n4+1, ... in depth (= node index) order; the last segment scores them.
+  const int nscr = last ? __popcll(csa_mask) : 0;
+  if (last) {
+    // Wave w takes entries w, w + 8, ...; lane (h8, c) holds channels
+    // 8c..8c+7 of head h0 + h8, for head groups h0.
+    for (int t = wv; t < nscr; t += kTkNW) {
+      uint64_t x = csa_mask;
+      for (int u = 0; u < t; ++u) x &= x - 1;
+      const int nd = __ffsll((unsigned long long)x) - 1;  // the t-th path node closing a CSA block
+      const uint4 kv = *reinterpret_cast<const uint4 *>(scr_c4 + ((int64_t)b * d.D + nd) * d_u + d.d_row + 8 * cc);
       float sum = 0.f;
       for (int h0 = 0; h0 < d.H_idx; h0 += 8) {
         const int h = h0 + hl;
         float part = 0.f, wh = 0.f;
         if (h < d.H_idx) {
-          const uint4 qv = *reinterpret_cast<const uint4 *>(q_idx + (node * d.H_idx + h) * 64 + 8 * cc);
+          const uint4 qv =
+              h0 == 0 ? qv0 : *reinterpret_cast<const uint4 *>(q_idx + (node * d.H_idx + h) * 64 + 8 * cc);
           part = dot8_bf16(qv, kv);
-          wh = bf2f(w_idx[node * d.H_idx + h]);
+          wh = h0 == 0 ? wh0 : bf2f(w_idx[node * d.H_idx + h]);
         }
         part += __shfl_xor(part, 1, 64);
         part += __shfl_xor(part, 2, 64);
@@ -143,263 +355,149 @@ __global__ void __launch_bounds__(kNT) topk_kernel(tv_dims d, CacheView c, const
       if (lane == 0) scr_score[t] = sum;
     }
   }
-  __syncthreads();
-
-  const int n = n4 + nscr;
-  int32_t *out = sel + node * d.topk;
-  const float *sc = scores + node * score_stride;
-  if (n <= d.topk) {
-    for (int t = tid; t < d.topk; t += kNT) out[t] = t < n ? t : -1;
-  } else {
-    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-    if constexpr (kLds) {
-      // Keys into LDS in 16-byte groups, with their extremes.  Score rows are
-      // 256-byte aligned and padded to a multiple of 64 entries, so whole
-      // float4 groups of the committed part can be read.
-      const int n4v = (n4 + 3) >> 2;
-      const float4 *sc4 = reinterpret_cast<const float4 *>(sc);
-      uint4 *keys4 = reinterpret_cast<uint4 *>(keys);
-      for (int j0 = 0; j0 < n4v; j0 += kNT * 8) {  // eight float4 loads in flight per thread
-        float4 v[8];
+  lds_barrier();  // path, hca_node and the path-entry scores are visible
+  const int seg_n = cn + nscr;  // path entries follow the committed ones of the last segment
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = j0 + tid + kNT * u;
-          v[u] = j < n4v ? sc4[j] : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = j0 + tid + kNT * u;
-          if (j < n4v) {
-            const float f[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-            uint32_t k[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int s = 4 * j + e;
-              k[e] = score_key(s < n4 ? f[e] : (s < n ? scr_score[s - n4] : 0.f));
-              if (s < n) {
-                kmin = min(kmin, k[e]);
-                kmax = max(kmax, k[e]);
-              }
-            }
-            keys4[j] = make_uint4(k[0], k[1], k[2], k[3]);
-          }
-        }
-      }
-      // path entries beyond the last group of committed ones
-      const int s = 4 * n4v + tid;
-      if (s < n) {
-        const uint32_t k = score_key(scr_score[s - n4]);
-        keys[s] = k;
-        kmin = min(kmin, k);
-        kmax = max(kmax, k);
-      }
-    } else {
-      for (int s0 = 0; s0 < n; s0 += kNT * 8) {
-        float v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int s = s0 + tid + kNT * u;
-          v[u] = s < n4 ? sc[s] : (s < n ? scr_score[s - n4] : 0.f);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (s0 + tid + kNT * u < n) {
-            const uint32_t k = score_key(v[u]);
-            kmin = min(kmin, k);
-            kmax = max(kmax, k);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
-      kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
-    }
-    if (lane == 0) {
-      mm[0][wv] = kmin;
-      mm[1][wv] = kmax;
-    }
-    __syncthreads();
-    kmin = mm[0][0];
-    kmax = mm[1][0];
-#pragma unroll
-    for (int w = 1; w < kNW; ++w) {
-      kmin = min(kmin, mm[0][w]);
-      kmax = max(kmax, mm[1][w]);
-    }
-
-    // Radix select of the topk-th largest key.  After it, keys whose masked
-    // bits exceed `prefix` are taken, and of those equal to it the `remaining`
-    // lowest-index ones.  A pass whose chosen bin holds exactly `remaining`
-    // keys ends the search: all of them are taken.
-    uint32_t prefix = kmin, pmask = 0xFFFFFFFFu;
-    int remaining = d.topk;
-    if (kmin != kmax) {
-      const int hb = 31 - __clz(kmin ^ kmax);
-      const uint32_t low = (hb == 31) ? 0xFFFFFFFFu : ((2u << hb) - 1u);
-      pmask = ~low;
-      prefix = kmin & pmask;
-      const int slot = lane & (kCopies - 1);
-      for (int top = hb; top >= 0;) {
-        const int nb = top + 1 < 8 ? top + 1 : 8;
-        const int sh = top + 1 - nb;
-        const uint32_t dmask = (1u << nb) - 1u;
-        for (int t = tid; t < 256 * kCopies / 4; t += kNT) reinterpret_cast<uint4 *>(hist)[t] = make_uint4(0, 0, 0, 0);
-        __syncthreads();
-        auto count = [&](uint32_t k, bool ok) {
-          if (ok && (k & pmask) == prefix) atomicAdd(&hist[((k >> sh) & dmask) * kCopies + slot], 1u);
-        };
-        if constexpr (kLds) {
-          const int nv = (n + 3) >> 2;
-          const uint4 *keys4 = reinterpret_cast<const uint4 *>(keys);
-          for (int j0 = 0; j0 < nv; j0 += kNT * 8) {
-            uint4 kk[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) kk[u] = keys4[min(j0 + tid + kNT * u, nv - 1)];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int s = 4 * (j0 + tid + kNT * u);
-              count(kk[u].x, s + 0 < n);
-              count(kk[u].y, s + 1 < n);
-              count(kk[u].z, s + 2 < n);
-              count(kk[u].w, s + 3 < n);
-            }
-          }
-        } else {
-          for (int s0 = 0; s0 < n; s0 += kNT * 8) {
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              const int s = s0 + tid + kNT * u;
-              v[u] = s < n4 ? sc[s] : (s < n ? scr_score[s - n4] : 0.f);
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) count(score_key(v[u]), s0 + tid + kNT * u < n);
-          }
-        }
-        __syncthreads();
-        if (wv == 0) {  // lane owns bins 255-4l .. 252-4l, scanned from the top bin down
-          const uint4 *h4 = reinterpret_cast<const uint4 *>(hist) + (252 - 4 * lane) * (kCopies / 4);
-          int cntv[4], local = 0;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {  // bin 255 - 4l - u
-            const uint4 a = h4[(3 - u) * 2], bq = h4[(3 - u) * 2 + 1];
-            cntv[u] = (int)(a.x + a.y + a.z + a.w + bq.x + bq.y + bq.z + bq.w);
-            local += cntv[u];
-          }
-          int incl = local;
-#pragma unroll
-          for (int o = 1; o < 64; o <<= 1) {
-            const int y = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += y;
-          }
-          int above = incl - local;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            if (above < remaining && remaining <= above + cntv[u]) {
-              found[0] = 255 - 4 * lane - u;
-              found[1] = above;
-              found[2] = cntv[u];
-            }
-            above += cntv[u];
-          }
-        }
-        __syncthreads();
-        prefix |= found[0] << sh;
-        pmask |= dmask << sh;
-        remaining -= (int)found[1];
-        if ((int)found[2] == remaining) break;
-        top -= nb;
-      }
-    }
-
-    // Ordered compaction: wave w owns a contiguous index range.  A counting
-    // sweep gives every wave the numbers of greater and equal keys before its
-    // range; a second sweep writes each taken index at (greater before it) +
-    // min(equal before it, remaining).
-    auto key_at = [&](int s) -> uint32_t {  // 0 <= s < n
-      if constexpr (kLds) return keys[s];
-      else return score_key(s < n4 ? sc[s] : scr_score[s - n4]);
-    };
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int seg = (n + kNT - 1) / kNT * 64;
-    const int lo = wv * seg, hi = std::min(n, lo + seg);
-    int cgt = 0, ceq = 0;
-    for (int s0 = lo; s0 < hi; s0 += 256) {
-      uint32_t kk[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) kk[u] = key_at(min(s0 + 64 * u + lane, n - 1));
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const bool ok = s0 + 64 * u + lane < hi;
-        const uint32_t km = kk[u] & pmask;
-        cgt += __popcll(__ballot(ok && km > prefix));
-        ceq += __popcll(__ballot(ok && km == prefix));
-      }
-    }
-    if (lane == 0) {
-      wcnt[0][wv] = cgt;
-      wcnt[1][wv] = ceq;
-    }
-    __syncthreads();
-    int gt_before = 0, eq_before = 0;
-    for (int w = 0; w < wv; ++w) {
-      gt_before += wcnt[0][w];
-      eq_before += wcnt[1][w];
-    }
-    for (int s0 = lo; s0 < hi; s0 += 256) {
-      uint32_t kk[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) kk[u] = key_at(min(s0 + 64 * u + lane, n - 1));
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int s = s0 + 64 * u + lane;
-        const bool ok = s < hi;
-        const uint32_t km = kk[u] & pmask;
-        const bool gt = ok && km > prefix, eq = ok && km == prefix;
-        const uint64_t bgt = __ballot(gt), beq = __ballot(eq);
-        const int g = gt_before + __popcll(bgt & lt_mask);
-        const int e = eq_before + __popcll(beq & lt_mask);
-        if (gt) out[g + std::min(e, remaining)] = s;
-        else if (eq && e < remaining) out[g + e] = s;
-        gt_before += __popcll(bgt);
-        eq_before += __popcll(beq);
-      }
-    }
+  for (int j = 0; j < kTkKPT; ++j) {
+    const int e = tid + kTkNT * j;
+    const float sv =
+        e < cn ? __uint_as_float(key[j]) : scr_score[std::min(std::max(e - cn, 0), kMaxScratch - 1)];
+    key[j] = e < seg_n ? live_key(sv) : 0u;
   }
 
-  // The node's key list for the attention kernel: latent-row pointers of its
-  // selected CSA entries, HCA entries, window rows and path rows, in the
-  // order the attention enumerates them.  The selection list written above is
-  // read back by this workgroup after the barrier.
-  __syncthreads();
-  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  {
-    const uint16_t **tab = keytab + node * keytab_stride;
-    const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
-    for (int t = tid; t < nk.n_keys; t += kNT)
-      tab[t] = key_row(d, nk, b, t, out, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128, tree_u);
+  // The node's key table: non-CSA keys here, selected CSA entries below.
+  const uint16_t **tab = keytab + node * keytab_stride;
+  if (seg == 0) {
+    for (int t = nk.nsel + tid; t < nk.n_keys; t += kTkNT)
+      tab[t] = key_row(d, nk, b, t, nullptr, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128,
+                       tree_u);
     if (tid == 0) nkeys_tab[node] = nk.n_keys;
   }
+
+  // Select: the taken elements in element order, list[t] (t < taken) in LDS,
+  // or every element when the segment holds at most k.
+  const int k = d.topk;
+  const bool all = seg_n <= k;
+  const int taken = all ? seg_n : k;
+  if (!all) {
+    uint32_t prefix, pmask;
+    int remaining;
+    radix_threshold<kTkKPT>(key, seg_n, k, sh, prefix, pmask, remaining);
+    compact_taken<kTkKPT>(key, seg_n, prefix, pmask, remaining, sh);
+  }
+  const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
+  if (nseg == 1) {
+    // the node's selection (ascending, -1 padded) and its CSA key pointers
+    int32_t *out = sel + node * k;
+    for (int t = tid; t < k; t += kTkNT) {
+      const int s = t < taken ? (all ? t : list[t]) : -1;  // one segment: element index = logical index
+      out[t] = s;
+      if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, scr_c4);
+    }
+  } else {
+    // survivors of this segment, in index order, then padding, for the merge
+    const int64_t sv = ((int64_t)node * max_seg + seg) * k;
+    for (int t = tid; t < k; t += kTkNT) {
+      const int e = t < taken ? (all ? t : list[t]) : -1;
+      surv_idx[sv + t] = e < 0 ? -1 : (e < cn ? c0 + e : n4 + (e - cn));
+      surv_key[sv + t] = e < 0 ? 0u : live_key(e < cn ? sc[e] : scr_score[e - cn]);
+    }
+    if (tid == 0) surv_cnt[node * max_seg + seg] = taken;
+  }
+}
+
+// Merge of a segmented node: the topk of the survivors of all its segments.
+// Segment s holds k slots (survivors in index order, then padding key 0), so
+// the slots of all segments in order list the survivors in index order.
+__global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheView c, const uint64_t *__restrict__ anc,
+                                                           const int32_t *__restrict__ depth,
+                                                           const uint16_t *__restrict__ scr_c4,
+                                                           int32_t *__restrict__ sel,
+                                                           const int32_t *__restrict__ row_status,
+                                                           const uint16_t **__restrict__ keytab, int keytab_stride,
+                                                           int max_seg, const int32_t *__restrict__ surv_idx,
+                                                           const uint32_t *__restrict__ surv_key,
+                                                           const int32_t *__restrict__ surv_cnt) {
+  __shared__ SelShared sh;
+  __shared__ int real_cnt;
+  __shared__ int32_t path[64], hca_node[64], cnt[2];
+  const int tid = threadIdx.x;
+  const int64_t node = blockIdx.x;
+  const int b = (int)(node / d.D);
+  const int i = (int)(node - (int64_t)b * d.D);
+  if (row_status[b] != TV_ROW_OK) return;
+  const int32_t L = c.len[b];
+  if (!len_ok(L, d.max_len)) return;
+  const int n4 = L / d.ratio_csa;
+  const int nseg = topk_segments(n4);
+  if (nseg <= 1) return;
+  const int k = d.topk;
+  if (tid == 0) {
+    int run = 0;
+    for (int s = 0; s < nseg; ++s) run += surv_cnt[node * max_seg + s];
+    real_cnt = run;
+  }
+  const int slots = nseg * k;
+  const int64_t sv = (int64_t)node * max_seg * k;
+  uint32_t key[kTopkMergeKPT];
+#pragma unroll
+  for (int j = 0; j < kTopkMergeKPT; ++j) {
+    const int e = tid + kTkNT * j;
+    const uint32_t kk = surv_key[sv + std::min(e, slots - 1)];
+    key[j] = e < slots ? kk : 0u;
+  }
+  __syncthreads();
+  const int total = real_cnt;
+  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
+  const uint16_t **tab = keytab + node * keytab_stride;
+  const int64_t c4b = c.c4_base[b];
+  int32_t *out = sel + node * k;
+  const bool all = total <= k;  // every real survivor (key above 0) is taken
+  uint32_t prefix = 0u, pmask = 0xFFFFFFFFu;
+  int remaining = 0;
+  if (!all) radix_threshold<kTopkMergeKPT>(key, slots, k, sh, prefix, pmask, remaining);
+  compact_taken<kTopkMergeKPT>(key, slots, prefix, pmask, remaining, sh);
+  const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
+  const int taken = all ? total : k;
+  for (int t = tid; t < k; t += kTkNT) {
+    const int s = t < taken ? surv_idx[sv + list[t]] : -1;
+    out[t] = s;
+    if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, scr_c4);
+  }
+}
+
+int topk_max_segments(const tv_dims &d) {
+  const int64_t n4 = (int64_t)d.max_len / d.ratio_csa;
+  return n4 <= kTopkSeg ? 1 : (int)((n4 + kTopkSeg - 1) / kTopkSeg);
+}
+
+bool topk_supported(const tv_dims &d) {
+  const int s = topk_max_segments(d);
+  return d.topk <= kTkBins && (s == 1 || (s <= kTopkMaxSeg && (int64_t)s * d.topk <= kTopkMergeCap));
 }
 
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
                        int32_t *row_status, int32_t *row_order, const uint16_t **keytab, int32_t keytab_stride,
-                       int32_t *nkeys, hipStream_t s) {
-  if (d.D > kMaxScratch) return hipErrorInvalidValue;
-  // the LDS variant serves every node when the longest candidate list fits
-  const int64_t max_n = (int64_t)d.max_len / d.ratio_csa + d.D;
-  if (max_n <= kLdsKeys)
-    topk_kernel<true><<<d.B * d.D, kNT, 0, s>>>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
-                                                score_stride, sel, row_status, row_order, keytab, keytab_stride,
-                                                nkeys);
-  else
-    topk_kernel<false><<<d.B * d.D, kNT, 0, s>>>(d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
-                                                 score_stride, sel, row_status, row_order, keytab, keytab_stride,
-                                                 nkeys);
+                       int32_t *nkeys, int32_t *surv_idx, uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s) {
+  if (d.D > kMaxScratch || !topk_supported(d)) return hipErrorInvalidValue;
+  const int max_seg = topk_max_segments(d);
+  topk_kernel<<<(unsigned)((int64_t)d.B * d.D * max_seg), kTkNT, 0, s>>>(
+      d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores, score_stride, sel, row_status, row_order,
+      keytab, keytab_stride, nkeys, max_seg, surv_idx, surv_key, surv_cnt);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
+                             const uint16_t *scr_c4, int32_t *sel, const int32_t *row_status,
+                             const uint16_t **keytab, int32_t keytab_stride, const int32_t *surv_idx,
+                             const uint32_t *surv_key, const int32_t *surv_cnt, hipStream_t s) {
+  const int max_seg = topk_max_segments(d);
+  if (max_seg <= 1) return hipSuccess;
+  topk_merge_kernel<<<(unsigned)((int64_t)d.B * d.D), kTkNT, 0, s>>>(d, c, anc, depth, scr_c4, sel, row_status,
+                                                                     keytab, keytab_stride, max_seg, surv_idx,
+                                                                     surv_key, surv_cnt);
   return hipGetLastError();
 }
 

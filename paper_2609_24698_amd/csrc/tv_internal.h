@@ -20,6 +20,16 @@ struct CacheView {
 // Keys one attention workgroup takes per split (its LDS pointer table).
 constexpr int kAttnMaxChunk = 1280;
 
+// CSA top-k: committed entries one workgroup selects among (longer nodes are
+// cut into segments of this many entries and merged), and the survivors the
+// merge holds (512 threads x kTopkMergeKPT keys).
+constexpr int kTopkSeg = 512 * 33;
+constexpr int kTopkMergeKPT = 68;
+constexpr int kTopkMergeCap = 512 * kTopkMergeKPT;
+constexpr int kTopkMaxSeg = 64;
+int topk_max_segments(const tv_dims &d);
+bool topk_supported(const tv_dims &d);
+
 // How the verify attention splits a node's keys across workgroups.
 struct SplitPlan {
   int32_t max_keys;   // upper bound of any node's key count
@@ -36,6 +46,9 @@ struct WsLayout {
   size_t row_order;   // int32 [B]: rows by committed length, longest first
   size_t keytab;      // const uint16_t* [B*D][plan.max_keys]: latent row of every key of every node
   size_t nkeys;       // int32 [B*D]: key count of every node
+  size_t surv_idx;    // int32 [B*D][topk segments][topk]: survivors of each top-k segment (segmented nodes only)
+  size_t surv_key;    // uint32, same shape: their score keys
+  size_t surv_cnt;    // int32 [B*D][topk segments]
   size_t total;
   int32_t score_stride;
   SplitPlan plan;
@@ -56,7 +69,11 @@ hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tre
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
                        int32_t *row_status, int32_t *row_order, const uint16_t **keytab, int32_t keytab_stride,
-                       int32_t *nkeys, hipStream_t s);
+                       int32_t *nkeys, int32_t *surv_idx, uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s);
+hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
+                             const uint16_t *scr_c4, int32_t *sel, const int32_t *row_status,
+                             const uint16_t **keytab, int32_t keytab_stride, const int32_t *surv_idx,
+                             const uint32_t *surv_key, const int32_t *surv_cnt, hipStream_t s);
 hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
                        const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
                        float *part_ml, uint16_t *out, float *lse, hipStream_t s);

@@ -77,6 +77,28 @@ def test_c4_full_size():
     _full("C4", [0])
 
 
+@pytest.mark.parametrize("topk,zero_w", [(512, False), (2048, False), (512, True)],
+                         ids=["k512", "k2048", "k512-all-ties"])
+def test_segmented_topk(topk, zero_w):
+    """Rows longer than one top-k segment (16,896 candidates): every segment
+    keeps its own top-k and a merge selects among the survivors.  Row 0 has
+    three segments, row 1 two.  With zero indexer weights on two nodes every
+    score ties at 0 and the selection is the lowest logical indices across
+    segment boundaries."""
+    w = synth.make_workload("C1", B=2, D=8, lens=[140001, 70000], seed=75, topk=topk)
+    if zero_w:
+        w.w_idx[0, 3] = 0
+        w.w_idx[1, 5] = 0
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    ref = O.run_round(w, nodes)
+    r = _device(w)
+    stats = _check_stages(w, ref, r, nodes, rerun=_rerun(w, ref))
+    _say(f"  segmented top-k k={topk} zero_w={zero_w}: {stats}")
+    if zero_w:
+        sel = r.host("sel")
+        assert np.array_equal(sel[0, 3], np.arange(topk)) and np.array_equal(sel[1, 5], np.arange(topk))
+
+
 def _small(B=5, D=8, lens=(1003, 2047, 999, 1023, 1500), seed=71, **over):
     return synth.make_workload("C1", B=B, D=D, lens=list(lens), seed=seed, topk=64, **over)
 
