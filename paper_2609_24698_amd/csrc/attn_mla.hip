@@ -364,8 +364,12 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
     }
     lds_barrier();
     lds_barrier();  // sums and references published
-    // Epilogue: lane holds, per head tile t, head 32 t + l32 and value
-    // channels 128 pq + 32 ct + 8 (j / 4) + 4 hi + (j % 4).
+    // Epilogue through LDS (the K buffers are free): lane holds, per head
+    // tile t, head 32 t + l32 and value channels 128 pq + 32 ct + 8 (j / 4) +
+    // 4 hi + (j % 4).  The wave writes its block as rows [head][128 channels]
+    // (bf16, 256-byte rows; float32, 512-byte rows for a split's partial),
+    // 16-byte chunks XOR-swizzled by head, then stores each row contiguously.
+    unsigned char *ob = &sK[0][0] + pq * (single ? 64 * 256 : 64 * 512);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int h = t * 32 + l32;
@@ -374,19 +378,33 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
-          const int col = 128 * pq + 32 * ct + 8 * jq + 4 * hi;
+          const int c = 32 * ct + 8 * jq + 4 * hi;  // channel within this wave's 128
           const float v0 = acc_o[t][ct][4 * jq] * inv, v1 = acc_o[t][ct][4 * jq + 1] * inv;
           const float v2 = acc_o[t][ct][4 * jq + 2] * inv, v3 = acc_o[t][ct][4 * jq + 3] * inv;
           if (single) {
             uint2 w;
             w.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v0, v1}, bf16x2));
             w.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v2, v3}, bf16x2));
-            *reinterpret_cast<uint2 *>(out + (node * kH + h) * kDV + col) = w;
+            *reinterpret_cast<uint2 *>(ob + h * 256 + (((c >> 3) ^ (h & 15)) << 4) + ((c >> 2) & 1) * 8) = w;
           } else {
-            *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * kH + h) * kDV + col) =
-                make_float4(v0, v1, v2, v3);
+            *reinterpret_cast<float4 *>(ob + h * 512 + (((c >> 2) ^ (h & 31)) << 4)) = make_float4(v0, v1, v2, v3);
           }
         }
+    }
+    if (single) {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {  // rows 4u .. 4u+3, sixteen 16-byte chunks each
+        const int r = 4 * u + (lane >> 4), ch = lane & 15;
+        const uint4 v = *reinterpret_cast<const uint4 *>(ob + r * 256 + ((ch ^ (r & 15)) << 4));
+        *reinterpret_cast<uint4 *>(out + (node * kH + r) * kDV + 128 * pq + 8 * ch) = v;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 32; ++u) {  // rows 2u, 2u+1, thirty-two 16-byte chunks each
+        const int r = 2 * u + (lane >> 5), ch = lane & 31;
+        const float4 v = *reinterpret_cast<const float4 *>(ob + r * 512 + ((ch ^ (r & 31)) << 4));
+        *reinterpret_cast<float4 *>(part_o + (((node * splits) + split) * kH + r) * kDV + 128 * pq + 4 * ch) = v;
+      }
     }
   }
 }
