@@ -24,9 +24,12 @@
 // and the transpose reads are free of bank conflicts.
 //
 // The probabilities use a fixed reference per head (the first tile's
-// maximum), so the output accumulators are never rescaled; a logit more than
-// 64 (log2 units) above it restarts the split from the largest logit seen,
-// at most kMaxRestarts times.  A node whose keys fit one split writes its
+// maximum), so the output accumulators are never rescaled; if any logit of
+// the split ends up more than 64 (log2 units) above it, the split runs again
+// from the largest logit seen, at most kMaxRestarts times.  Each head's
+// probability sum is the product of P^T with a value operand of ones (one
+// value wave, four products per tile), so the sums cover exactly the bf16
+// probabilities the value contraction uses.  A node whose keys fit one split writes its
 // normalised output; otherwise each split writes an unnormalised partial
 // (O, reference, sum) that the combine kernel merges.
 #include "attn_common.h"
@@ -43,7 +46,8 @@ constexpr int kGB = kKT * 128;            // bytes of one column group of a tile
 constexpr int kTB = kGroups * kGB;        // bytes of a tile
 constexpr int kNBUF = 4;                  // K tile buffers
 constexpr int kPSlots = 8;                // key-pointer table slots (one tile each)
-constexpr int kG0 = 5;                    // column groups copied by w4 (w5 copies the rest)
+// Column groups each wave copies: w4 groups 0..2, w5 3..5, w3 6..7, w2 8 (the
+// rope group); the value waves w2, w3 have the most idle time per tile.
 constexpr float kSlack = 64.0f;
 constexpr int kMaxRestarts = 8;
 static_assert(kDV == 128 * 4, "four value waves of 128 channels");
@@ -87,9 +91,10 @@ __device__ __forceinline__ void vm_wait_n(int n) {
   switch (n) {
     case 0: vm_wait<0>(); break;
     case 1: vm_wait<1>(); break;
-    case 4 * (mla::kGroups - mla::kG0): vm_wait<4 * (mla::kGroups - mla::kG0)>(); break;
-    case 4 * mla::kG0: vm_wait<4 * mla::kG0>(); break;
-    case 4 * mla::kG0 + 1: vm_wait<4 * mla::kG0 + 1>(); break;
+    case 4: vm_wait<4>(); break;
+    case 8: vm_wait<8>(); break;
+    case 12: vm_wait<12>(); break;
+    case 13: vm_wait<13>(); break;
     default: vm_wait<0>(); break;
   }
 }
@@ -103,7 +108,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   __shared__ __attribute__((aligned(1024))) unsigned char sK[kNBUF][kTB];
   __shared__ __attribute__((aligned(16))) unsigned char sP[2][kH * 64];
   __shared__ __attribute__((aligned(16))) const uint16_t *sPtr[kPSlots][kKT];
-  __shared__ int sFlag[2][2];
+  __shared__ int sOver[2];
   __shared__ float sSum[kH];
   __shared__ float sRef[kH];
 
@@ -123,7 +128,76 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   const int T = (nkeys + kKT - 1) / kKT;
   const bool single = n_keys <= chunk;
   const float sl2 = d.scale * kLog2e;
-  auto overflowed = [&](int it) { return (sFlag[it & 1][0] | sFlag[it & 1][1]) != 0; };
+  // Every role runs the same barrier sequence per attempt: two in the
+  // prologue, one per iteration but the last, two at the end (E1: loop done;
+  // E2: overflow verdict, sums and references published), and one more before
+  // a restart.  A restart is decided once per attempt, from the largest logit
+  // each logit wave saw: any head more than kSlack above its reference.
+  auto restart_now = [&](int attempt) { return (sOver[0] | sOver[1]) != 0 && attempt < kMaxRestarts; };
+
+  // Direct copies of key rows into the tile buffers.  The copying waves and
+  // their column groups: w4 0..2, w5 3..5, w3 6..7, w2 8.
+  const int g_lo = wv == 4 ? 0 : wv == 5 ? 3 : wv == 3 ? 6 : wv == 2 ? 8 : 0;
+  const int g_hi = wv == 4 ? 3 : wv == 5 ? 6 : wv == 3 ? 8 : wv == 2 ? 9 : 0;
+  const int n_g = 4 * (g_hi - g_lo);
+  const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+  const uint32_t lds_k = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
+  const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
+  // Pointer table of tile u (w4 only): lane l copies 4 bytes (half l & 1) of
+  // the pointer of key min(32 u + l / 2, nkeys - 1), so rows past the
+  // split's end repeat its last key (finite data; their probabilities are 0).
+  auto copy_ptrs = [&](int u) {
+    const int r = std::min(u * kKT + (lane >> 1), nkeys - 1);
+    dma4(reinterpret_cast<const unsigned char *>(tab + r) + 4 * (lane & 1), lds_p + (u % kPSlots) * (kKT * 8));
+  };
+  // Rows of tile u into buffer u % 4: instruction (g, k) fills rows 8k ..
+  // 8k+7 of group g (lane = row-in-8 * 8 + slot); slot s of row r holds
+  // logical chunk slot(r, s) of the group.  All source addresses are formed
+  // before the first copy is issued.
+  auto copy_tile = [&](int u) {
+    const unsigned char *src[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int r = 8 * k + (lane >> 3);
+      src[k] = reinterpret_cast<const unsigned char *>(sPtr[u % kPSlots][r]) + slot(r, lane & 7) * 16;
+    }
+    const uint32_t dst = lds_k + (u % kNBUF) * kTB;
+    const unsigned char *a[3][4];
+#pragma unroll
+    for (int gg = 0; gg < 3; ++gg)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) a[gg][k] = src[k] + (g_lo + gg) * 128;
+#pragma unroll
+    for (int gg = 0; gg < 3; ++gg)
+      if (g_lo + gg < g_hi)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dma16(a[gg][k], dst + (g_lo + gg) * kGB + k * 1024);
+  };
+  // The copying waves' share of an attempt's prologue and of iteration it.
+  auto copy_prologue = [&]() {
+    if (wv == 4) {
+      for (int u = 0; u < std::min(T, 5); ++u) copy_ptrs(u);
+      vm_wait<0>();
+    }
+    lds_barrier();  // pointer tables of tiles 0..4 copied
+    if (n_g) {
+      copy_tile(0);
+      if (T > 1) copy_tile(1);
+    }
+    vm_wait_n(T > 1 ? n_g : 0);
+  };
+  auto copy_step = [&](int it) {  // issue tile it+3 (and pointers of tile it+6); returns copies issued
+    int n = 0;
+    if (wv == 4 && it + 6 < T) {
+      copy_ptrs(it + 6);
+      n += 1;
+    }
+    if (n_g && it + 3 < T) {
+      copy_tile(it + 3);  // buffer (it+3) % 4 held tile it-1, read before the last barrier
+      n += n_g;
+    }
+    return n;
+  };
 
   if (wv == 0 || wv == 1) {
     // ---- logit wave: heads 32 hh .. 32 hh + 31 ------------------------------
@@ -143,7 +217,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
     for (int c = 0; c < 4; ++c) kofs[c] = l32 * 128 + slot(l32, 2 * c + hi) * 16;
     const int pw0 = p_off(head, hi), pw1 = p_off(head, 2 + hi);
 
-    float m_ref = -INFINITY, m_seen = -INFINITY, l_run = 0.f;
+    float m_ref = -INFINITY, m_seen = -INFINITY;
     // Complete logits of the tile's 32 keys x this wave's 32 heads: two
     // accumulator chains (even and odd k-steps), key reads six ahead.
     auto qk_tile = [&](int tile) {
@@ -167,7 +241,8 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       return s0 + s1;
     };
     // Element v of a lane's logits is key 8 (v / 4) + 4 hi + v % 4 of the
-    // tile; keys past the split are -inf.
+    // tile; keys past the split are -inf.  Probabilities against the reference
+    // go to LDS as bf16 P^T; their sums come from the value contraction.
     auto process = [&](int tile, f32x16 s, bool first) {
       const int nvalid = nkeys - tile * kKT;
       if (nvalid < kKT) {
@@ -181,14 +256,9 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       mx *= sl2;
       if (first) m_ref = fmaxf(mx, __shfl_xor(mx, 32, 64));  // the reference: the first tile's maximum
       m_seen = fmaxf(m_seen, mx);
-      const bool over = mx > m_ref + kSlack;
       float p[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], sl2, -m_ref));
-      float ls = 0.f;
-#pragma unroll
-      for (int v = 0; v < 16; v += 4) ls += (p[v] + p[v + 1]) + (p[v + 2] + p[v + 3]);
-      l_run += ls;
       uint4 c0, c1;
       c0.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[0], p[1]}, bf16x2));
       c0.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p[2], p[3]}, bf16x2));
@@ -201,35 +271,29 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       unsigned char *pt = sP[tile & 1];
       *reinterpret_cast<uint4 *>(pt + pw0) = c0;
       *reinterpret_cast<uint4 *>(pt + pw1) = c1;
-      const bool anyo = __any(over);
-      if (lane == 0) sFlag[tile & 1][hh] = anyo ? 1 : 0;
     };
 
     for (int attempt = 0;; ++attempt) {
-      l_run = 0.f;
       lds_barrier();  // pointer tables of the first tiles copied
       __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers
       lds_barrier();  // tile 0 landed
-      bool restart = false;
       for (int it = -1; it < T; ++it) {
-        if (it >= 0 && overflowed(it) && attempt < kMaxRestarts) {
-          restart = true;
-          break;
-        }
         if (it + 1 < T) process(it + 1, qk_tile(it + 1), it + 1 == 0 && attempt == 0);
         if (it == T - 1) break;
         lds_barrier();
       }
-      if (!restart) break;
-      lds_barrier();  // every wave has left the loop, copies drained
-      m_ref = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));  // restart from the largest logit seen
+      lds_barrier();  // E1
+      const float seen = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));
+      const bool over = __any(seen > m_ref + kSlack);
+      if (lane == 0) sOver[hh] = over ? 1 : 0;
+      if (hi == 0) sRef[head] = m_ref;
+      lds_barrier();  // E2
+      if (!restart_now(attempt)) break;
+      m_ref = seen;  // restart from the largest logit seen
+      lds_barrier();
     }
-    // Row sums per head: the two lanes of a head (fixed order).
-    const float lsum = l_run + __shfl_xor(l_run, 32, 64);
-    lds_barrier();
     if (hi == 0) {
-      sSum[head] = lsum;
-      sRef[head] = m_ref;
+      const float lsum = sSum[head];
       if (single) {
         if (lse) lse[node * kH + head] = (m_ref + __log2f(lsum)) * kLn2;
       } else {
@@ -237,75 +301,27 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
         part_ml[(((node * splits) + split) * kH + head) * 2 + 1] = lsum;
       }
     }
-    lds_barrier();
   } else if (wv == 4 || wv == 5) {
-    // ---- copy wave: column groups [g_lo, g_hi) of every tile -------------------
-    const int pr = wv - 4;
-    const int g_lo = pr ? kG0 : 0, g_hi = pr ? kGroups : kG0;
-    const int n_g = 4 * (g_hi - g_lo);
-    const uint16_t *const *tab = keytab + node * keytab_stride + k0;
-    const uint32_t lds_k = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
-    const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
-    // Pointer table of tile u: lane l copies 4 bytes (half l & 1) of the
-    // pointer of key min(32 u + l / 2, nkeys - 1), so rows past the split's
-    // end repeat its last key (finite data; their probabilities are 0).
-    auto copy_ptrs = [&](int u) {
-      const int r = std::min(u * kKT + (lane >> 1), nkeys - 1);
-      dma4(reinterpret_cast<const unsigned char *>(tab + r) + 4 * (lane & 1), lds_p + (u % kPSlots) * (kKT * 8));
-    };
-    // Rows of tile u into buffer u % 4: instruction (g, k) fills rows
-    // 8k .. 8k+7 of group g (lane = row-in-8 * 8 + slot); slot s of row r
-    // holds logical chunk slot(r, s) of the group.
-    auto copy_tile = [&](int u) {
-      const unsigned char *src[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int r = 8 * k + (lane >> 3);
-        src[k] = reinterpret_cast<const unsigned char *>(sPtr[u % kPSlots][r]) + slot(r, lane & 7) * 16;
-      }
-      const uint32_t dst = lds_k + (u % kNBUF) * kTB;
-      for (int g = g_lo; g < g_hi; ++g)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) dma16(src[k] + g * 128, dst + g * kGB + k * 1024);
-    };
-
+    // ---- copy wave ------------------------------------------------------------
     for (int attempt = 0;; ++attempt) {
-      if (pr == 0) {
-        for (int u = 0; u < std::min(T, 5); ++u) copy_ptrs(u);
-        vm_wait<0>();
-      }
-      lds_barrier();  // pointer tables of tiles 0..4 copied
-      copy_tile(0);
-      if (T > 1) copy_tile(1);
-      vm_wait_n(T > 1 ? n_g : 0);
+      copy_prologue();
       lds_barrier();  // tile 0 landed
-      bool restart = false;
       for (int it = -1; it < T; ++it) {
-        if (it >= 0 && overflowed(it) && attempt < kMaxRestarts) {
-          restart = true;
-          break;
-        }
-        int n = 0;
-        if (pr == 0 && it + 6 < T) {
-          copy_ptrs(it + 6);
-          n += 1;
-        }
-        if (it + 3 < T) {
-          copy_tile(it + 3);  // buffer (it+3) % 4 held tile it-1, read before the last barrier
-          n += n_g;
-        }
+        const int n = copy_step(it);
         if (it == T - 1) break;
         vm_wait_n(n);  // tile it+2 has landed (tile it+3 and the pointer table may still fly)
         lds_barrier();
       }
-      if (!restart) break;
       vm_wait<0>();
+      lds_barrier();  // E1
+      lds_barrier();  // E2
+      if (!restart_now(attempt)) break;
       lds_barrier();
     }
-    lds_barrier();
-    lds_barrier();
   } else {
     // ---- value wave: channels 128 pq .. 128 pq + 127 for all heads -------------
+    // Wave pq == 0 also accumulates each head's probability sum, as the
+    // product of P^T with a value operand of ones.
     const int pq = (wv & 1) | ((wv >> 2) << 1);
     const int g = lane >> 4, jj = lane & 15;
     // Transpose-read offsets: rows 16 ks + 8 s + 4 hi + jj/4, columns
@@ -317,7 +333,8 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       for (int ct = 0; ct < 4; ++ct)
         voff[rr][ct] = off(16 * (rr >> 1) + 8 * (rr & 1) + 4 * hi + (jj >> 2),
                            128 * pq + 32 * ct + 16 * (g & 1) + 4 * (jj & 3));
-    f32x16 acc_o[2][4];
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    f32x16 acc_o[2][4], acc_l[2];
     auto pv_tile = [&](int it) {
       const unsigned char *kt = sK[it % kNBUF];
       const unsigned char *pt = sP[it & 1];
@@ -327,7 +344,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
 #pragma unroll
         for (int t = 0; t < 2; ++t) pb[ks][t] = *reinterpret_cast<const bf16x8 *>(pt + p_off(32 * t + l32, 2 * ks + hi));
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) {
           const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
@@ -338,32 +355,38 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
           for (int t = 0; t < 2; ++t)
             acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks][t], acc_o[t][ct], 0, 0, 0);
         }
+        if (pq == 0)
+#pragma unroll
+          for (int t = 0; t < 2; ++t) acc_l[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pb[ks][t], acc_l[t], 0, 0, 0);
+      }
     };
 
     for (int attempt = 0;; ++attempt) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t) {
+        acc_l[t] = f32x16{};
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) acc_o[t][ct] = f32x16{};
-      lds_barrier();
-      lds_barrier();
-      bool restart = false;
+      }
+      copy_prologue();
+      lds_barrier();  // tile 0 landed
       for (int it = -1; it < T; ++it) {
-        if (it >= 0) {
-          if (overflowed(it) && attempt < kMaxRestarts) {
-            restart = true;
-            break;
-          }
-          pv_tile(it);
-        }
+        const int n = copy_step(it);
+        if (it >= 0) pv_tile(it);
         if (it == T - 1) break;
+        vm_wait_n(n);
         lds_barrier();
       }
-      if (!restart) break;
+      vm_wait<0>();
+      lds_barrier();  // E1
+      if (pq == 0 && hi == 0) {  // every row of the sums' accumulator holds the sum of its lane's head
+        sSum[l32] = acc_l[0][0];
+        sSum[32 + l32] = acc_l[1][0];
+      }
+      lds_barrier();  // E2
+      if (!restart_now(attempt)) break;
       lds_barrier();
     }
-    lds_barrier();
-    lds_barrier();  // sums and references published
     // Epilogue through LDS (the K buffers are free): lane holds, per head
     // tile t, head 32 t + l32 and value channels 128 pq + 32 ct + 8 (j / 4) +
     // 4 hi + (j % 4).  The wave writes its block as rows [head][128 channels]
