@@ -203,9 +203,9 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   // with m_ref fixed for the whole split (the first tile's maximum), so the
   // output accumulators are never rescaled inside the loop.  Probabilities may
   // reach 2^64 (exact in the float32 sums, relative precision kept in bf16).
-  // A logit more than 64 above the reference makes the workgroup restart the
-  // split from the larger maximum; each restart raises a reference by more
-  // than 64, and at most kMaxRestarts happen.
+  // If, at the end of the split, some head saw a logit more than 64 above its
+  // reference, the workgroup runs the split again from the largest logit
+  // seen (one verdict per attempt, at most kMaxRestarts).
   //
   // Work split of one tile: every wave of a head tile computes a partial S^T
   // over its k-steps; wave `part` then owns key rows 8 part + 4 hi + 0..3 (its
@@ -269,7 +269,6 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       lds_barrier();
       m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
     }
-    const bool over = mloc > m_ref + kSlack;
     const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[0], sl2, -m_ref));
     const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[1], sl2, -m_ref));
     const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[2], sl2, -m_ref));
@@ -279,7 +278,6 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
     pq.x = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
     pq.y = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p2, p3}, bf16x2));
     sP[ht][part][lane] = pq;
-    if (lane == 0) sFlag[wv] = __any(over) ? 1 : 0;
   };
   // O^T += V^T P^T for tile `it`, this wave's value channels, every head tile.
   // k-step ks covers key rows {16ks + 4hi + 0..3} (quarter 2ks) and
@@ -362,16 +360,9 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       // X phase: logits of tile it+1 first (their partials are published at
       // the end of the phase), then P V of tile it, whose products may still
       // be in the matrix pipeline during the next phase.
-      int anyf = 0;  // overflow flags of the probabilities of tile it
-#pragma unroll
-      for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
       if (it + 3 < ntiles) load_srcs(it + 3);  // copied in this phase (own copy) or the next
       if (more) qk_tile(it + 1);
       pv_tile(it);
-      if (anyf) {  // probabilities of tile it overflowed the reference
-        restart = attempt < kMaxRestarts;
-        if (restart) break;
-      }
       if constexpr (S::OWN) {  // this wave's reads of tile it are done: its groups of tile it+3 go there
         if (it + 3 < ntiles) issue_tile(it % NBUF);
       }
@@ -382,15 +373,25 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       wait_next(it + 1);
       lds_barrier();
     }
-    if (!restart) break;
-    // restart from the largest logit any quarter has seen, agreed through LDS
+    // One verdict per attempt: the largest logit each head saw, over its four
+    // quarters; any head more than kSlack above its reference runs the split
+    // again from that maximum.
     vm_wait<0>();
     __syncthreads();
     const float ms = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));
     if (hi == 0) sMx[ht][part][l32] = ms;
     __syncthreads();
-    m_ref = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
+    const float seen = fmaxf(fmaxf(sMx[ht][0][l32], sMx[ht][1][l32]), fmaxf(sMx[ht][2][l32], sMx[ht][3][l32]));
+    const bool over = __any(seen > m_ref + kSlack);  // the whole wave votes (not inside the lane-0 branch)
+    if (lane == 0) sFlag[wv] = over ? 1 : 0;
     __syncthreads();
+    int anyf = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) anyf |= sFlag[w];
+    restart = anyf != 0 && attempt < kMaxRestarts;
+    __syncthreads();
+    if (!restart) break;
+    m_ref = seen;
   }
   // Row sums and references per head tile: wave (ht, part) holds the sum over
   // its key quarter for head ht*32 + l32 (halves combined across hi).

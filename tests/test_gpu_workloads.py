@@ -99,6 +99,30 @@ def test_segmented_topk(topk, zero_w):
         assert np.array_equal(sel[0, 3], np.arange(topk)) and np.array_equal(sel[1, 5], np.arange(topk))
 
 
+@pytest.mark.parametrize("config", ["C1", "C0"])
+def test_softmax_restart(config):
+    """A committed window key whose logit exceeds the first tile's maximum by
+    far more than the fixed reference's slack (for many heads its first-pass
+    probability overflows float32): the split must run again from the largest
+    logit seen and still match the oracle.  Only key channels that are not
+    value channels are scaled (the shared latent's 64 rope channels; the
+    8-head shape's whole key), so the outputs keep their usual magnitude."""
+    w = synth.make_workload(config, B=2, D=8, lens=[6000, 3001], seed=76, topk=256, tree="random")
+    cap, d_k, v_off, d_v = w.dims["ring_cap"], w.dims["d_k"], w.dims["v_off"], w.dims["d_v"]
+    key_only = np.ones(d_k, dtype=bool)  # key channels that are not value channels
+    key_only[max(v_off, 0):min(v_off + d_v, d_k)] = False
+    for b in range(w.B):
+        L = int(w.lens[b])
+        row = O.bf16_to_f64(w.ring[b, (L - 1) % cap])
+        row[:d_k][key_only] *= 200.0 if config == "C1" else 100.0
+        w.ring[b, (L - 1) % cap] = O.f64_to_bf16(row)
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    ref = O.run_round(w, nodes)
+    r = _device(w)
+    stats = _check_stages(w, ref, r, nodes, rerun=_rerun(w, ref))
+    _say(f"  restart case: {stats}")
+
+
 def _small(B=5, D=8, lens=(1003, 2047, 999, 1023, 1500), seed=71, **over):
     return synth.make_workload("C1", B=B, D=D, lens=list(lens), seed=seed, topk=64, **over)
 
