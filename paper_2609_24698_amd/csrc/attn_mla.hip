@@ -93,7 +93,6 @@ __device__ __forceinline__ void vm_wait_n(int n) {
     case 1: vm_wait<1>(); break;
     case 4: vm_wait<4>(); break;
     case 8: vm_wait<8>(); break;
-    case 9: vm_wait<9>(); break;
     case 12: vm_wait<12>(); break;
     case 13: vm_wait<13>(); break;
     default: vm_wait<0>(); break;
@@ -130,16 +129,16 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   const bool single = n_keys <= chunk;
   const float sl2 = d.scale * kLog2e;
   // Every role runs the same barrier sequence per attempt: two in the
-  // prologue, one per iteration (it = -1 .. T-1), two at the end (E1: loop done;
+  // prologue, one per iteration but the last, two at the end (E1: loop done;
   // E2: overflow verdict, sums and references published), and one more before
   // a restart.  A restart is decided once per attempt, from the largest logit
   // each logit wave saw: any head more than kSlack above its reference.
   auto restart_now = [&](int attempt) { return (sOver[0] | sOver[1]) != 0 && attempt < kMaxRestarts; };
 
   // Direct copies of key rows into the tile buffers.  The copying waves and
-  // their column groups: w4 0..1, w5 2..3, w3 4..5, w2 6, w6 7, w7 8.
-  const int g_lo = wv == 4 ? 0 : wv == 5 ? 2 : wv == 3 ? 4 : wv == 2 ? 6 : wv == 6 ? 7 : wv == 7 ? 8 : 0;
-  const int g_hi = wv == 4 ? 2 : wv == 5 ? 4 : wv == 3 ? 6 : wv == 2 ? 7 : wv == 6 ? 8 : wv == 7 ? 9 : 0;
+  // their column groups: w4 0..2, w5 3..5, w3 6..7, w2 8.
+  const int g_lo = wv == 4 ? 0 : wv == 5 ? 3 : wv == 3 ? 6 : wv == 2 ? 8 : 0;
+  const int g_hi = wv == 4 ? 3 : wv == 5 ? 6 : wv == 3 ? 8 : wv == 2 ? 9 : 0;
   const int n_g = 4 * (g_hi - g_lo);
   const uint16_t *const *tab = keytab + node * keytab_stride + k0;
   const uint32_t lds_k = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
@@ -244,16 +243,18 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
     // Element v of a lane's logits is key 8 (v / 4) + 4 hi + v % 4 of the
     // tile; keys past the split are -inf.  Probabilities against the reference
     // go to LDS as bf16 P^T; their sums come from the value contraction.
-    auto process = [&](int tile, f32x16 s, bool first) {  // branch-free, so it interleaves with products
+    auto process = [&](int tile, f32x16 s, bool first) {
       const int nvalid = nkeys - tile * kKT;
+      if (nvalid < kKT) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[v] = 8 * (v >> 2) + 4 * hi + (v & 3) >= nvalid ? -INFINITY : s[v];
+        for (int v = 0; v < 16; ++v)
+          if (8 * (v >> 2) + 4 * hi + (v & 3) >= nvalid) s[v] = -INFINITY;
+      }
       float mx = s[0];
 #pragma unroll
       for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
       mx *= sl2;
-      const float mx2 = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      m_ref = first ? mx2 : m_ref;  // the reference: the first tile's maximum
+      if (first) m_ref = fmaxf(mx, __shfl_xor(mx, 32, 64));  // the reference: the first tile's maximum
       m_seen = fmaxf(m_seen, mx);
       float p[16];
 #pragma unroll
@@ -271,73 +272,16 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       *reinterpret_cast<uint4 *>(pt + pw0) = c0;
       *reinterpret_cast<uint4 *>(pt + pw1) = c1;
     };
-    // The products of tile tn and the probabilities of tile tc (logits s), in
-    // one issue order: a slice of the vector work follows each product, so it
-    // runs while the matrix core is busy (the same arithmetic as process()).
-    // Key reads go five products ahead; probabilities leave in 8-byte pieces.
-    auto step = [&](int tn, f32x16 s, int tc, bool first) {
-      const unsigned char *kt = sK[tn % kNBUF];
-      auto ka = [&](int ks) { return *reinterpret_cast<const bf16x8 *>(kt + (ks >> 2) * kGB + kofs[ks & 3]); };
-      bf16x8 a[6];
-#pragma unroll
-      for (int ks = 0; ks < 5; ++ks) a[ks] = ka(ks);
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
-      const int nvalid = nkeys - tc * kKT;
-      float mx = -INFINITY, mx2 = 0.f, pe = 0.f;
-      uint32_t c0 = 0;
-      unsigned char *pt = sP[tc & 1];
-#pragma unroll
-      for (int ks = 0; ks < kKS; ++ks) {
-        if (ks + 5 < kKS) a[(ks + 5) % 6] = ka(ks + 5);
-        if (ks & 1)
-          s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % 6], qf[ks], s1, 0, 0, 0);
-        else
-          s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % 6], qf[ks], s0, 0, 0, 0);
-        if (ks < 4) {  // mask and running maximum of elements 4 ks .. 4 ks + 3
-#pragma unroll
-          for (int v = 4 * ks; v < 4 * ks + 4; ++v) {
-            s[v] = 8 * (v >> 2) + 4 * hi + (v & 3) >= nvalid ? -INFINITY : s[v];
-            mx = fmaxf(mx, s[v]);
-          }
-        } else if (ks == 4) {
-          mx *= sl2;
-          mx2 = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        } else if (ks == 6) {
-          m_ref = first ? mx2 : m_ref;  // the reference: the first tile's maximum
-          m_seen = fmaxf(m_seen, mx);
-        } else if (ks >= 8 && ks < 24) {  // element ks - 8; every fourth completes 8 bytes of P
-          const int v = ks - 8;
-          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], sl2, -m_ref));
-          if (v & 1) {
-            const uint32_t cc = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pe, pv}, bf16x2));
-            if (v & 2)
-              *reinterpret_cast<uint2 *>(pt + (v < 8 ? pw0 : pw1) + ((v >> 2) & 1) * 8) = make_uint2(c0, cc);
-            else
-              c0 = cc;
-          } else {
-            pe = pv;
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      return s0 + s1;
-    };
 
     for (int attempt = 0;; ++attempt) {
       lds_barrier();  // pointer tables of the first tiles copied
       __builtin_amdgcn_s_waitcnt(0x0F70);  // queries are in registers
       lds_barrier();  // tile 0 landed
-      // Iteration it: the products of tile it+1 on the matrix cores while the
-      // vector units turn tile it's logits (held from the last iteration)
-      // into probabilities, which the value waves use in iteration it+1.
-      f32x16 s_cur = qk_tile(0);
-      lds_barrier();
-      for (int it = 0; it < T - 1; ++it) {
-        s_cur = step(it + 1, s_cur, it, it == 0 && attempt == 0);
+      for (int it = -1; it < T; ++it) {
+        if (it + 1 < T) process(it + 1, qk_tile(it + 1), it + 1 == 0 && attempt == 0);
+        if (it == T - 1) break;
         lds_barrier();
       }
-      process(T - 1, s_cur, T == 1 && attempt == 0);
-      lds_barrier();
       lds_barrier();  // E1
       const float seen = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));
       const bool over = __any(seen > m_ref + kSlack);
@@ -363,7 +307,9 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       copy_prologue();
       lds_barrier();  // tile 0 landed
       for (int it = -1; it < T; ++it) {
-        vm_wait_n(copy_step(it));  // tile it+2 has landed (tile it+3 and the pointer table may still fly)
+        const int n = copy_step(it);
+        if (it == T - 1) break;
+        vm_wait_n(n);  // tile it+2 has landed (tile it+3 and the pointer table may still fly)
         lds_barrier();
       }
       vm_wait<0>();
@@ -389,20 +335,8 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
                            128 * pq + 32 * ct + 16 * (g & 1) + 4 * (jj & 3));
     const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
     f32x16 acc_o[2][4], acc_l[2];
-    bf16x8 va[2][4];  // V^T operands of one tile, read an iteration before their products
-    auto read_v = [&](int it) {
+    auto pv_tile = [&](int it) {
       const unsigned char *kt = sK[it % kNBUF];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
-          const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
-          const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks + 1][ct]));
-          va[ks][ct] = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
-                                                      v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
-        }
-    };
-    auto pv_tile = [&](int it) {  // O^T += V^T P^T with the held V of tile it and P of tile it
       const unsigned char *pt = sP[it & 1];
       bf16x8 pb[2][2];
 #pragma unroll
@@ -412,10 +346,15 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
+        for (int ct = 0; ct < 4; ++ct) {
+          const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks][ct]));
+          const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(kt + voff[2 * ks + 1][ct]));
+          const bf16x8 va = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+                                                           v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
 #pragma unroll
           for (int t = 0; t < 2; ++t)
-            acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][ct], pb[ks][t], acc_o[t][ct], 0, 0, 0);
+            acc_o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks][t], acc_o[t][ct], 0, 0, 0);
+        }
         if (pq == 0)
 #pragma unroll
           for (int t = 0; t < 2; ++t) acc_l[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pb[ks][t], acc_l[t], 0, 0, 0);
@@ -433,12 +372,11 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
       lds_barrier();  // tile 0 landed
       for (int it = -1; it < T; ++it) {
         const int n = copy_step(it);
-        if (it >= 1) pv_tile(it - 1);  // P of tile it-1 was written in iteration it-1
-        if (it >= 0) read_v(it);       // tile it's buffer is refilled in iteration it+1
+        if (it >= 0) pv_tile(it);
+        if (it == T - 1) break;
         vm_wait_n(n);
         lds_barrier();
       }
-      pv_tile(T - 1);
       vm_wait<0>();
       lds_barrier();  // E1
       if (pq == 0 && hi == 0) {  // every row of the sums' accumulator holds the sum of its lane's head
