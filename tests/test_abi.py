@@ -53,6 +53,26 @@ def test_unsupported_shapes():
         assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == binding.TV_ERR_UNSUPPORTED
 
 
+# Top-k limits: topk at most 8192; a row of more than 16,896 candidates (ratio 4) is cut into segments, at most
+# 64 of them and segments x topk at most 34,816 (the 1M-token row with topk 2048: 16 segments, supported).
+TOPK_LIMITS = [
+    (dict(topk=8192), True), (dict(topk=8193), False),
+    (dict(topk=2048, max_len=1 << 20), True),
+    (dict(topk=4096, max_len=4 * 16896 * 9), False),   # 9 segments x 4096 > 34,816
+    (dict(topk=64, max_len=4 * 16896 * 64), True),     # 64 segments
+    (dict(topk=64, max_len=4 * 16896 * 64 + 4), False),  # 65 segments
+]
+
+
+@pytest.mark.parametrize("over,ok", TOPK_LIMITS, ids=lambda x: ",".join(f"{k}={v}" for k, v in x.items())
+                         if isinstance(x, dict) else str(x))
+def test_topk_limits_checked_without_gpu(over, ok):
+    lib = binding.lib()
+    d = _dims(**over)
+    want = binding.TV_ERR_INVALID_ARG if ok else binding.TV_ERR_UNSUPPORTED  # null pointers come after the dims
+    assert lib.tv_build_tree_mask(ctypes.byref(d), None, None, None, None, None) == want
+
+
 def test_null_pointers_rejected_without_gpu():
     lib = binding.lib()
     d = _dims()
