@@ -123,7 +123,23 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   const int k0 = split * chunk;
   const int32_t status = row_status[b];
   const int n_keys = nkeys_tab[node];
-  if (status != TV_ROW_OK || k0 >= n_keys) return;
+  // Pointer table of tile u (w4 only): lane l copies 4 bytes (half l & 1) of
+  // the pointer of key 32 u + l / 2, within the node's table row, so it needs
+  // no key count: the tiles 0..4 of the first attempt go out with the row's
+  // status and key count, one round trip earlier.
+  const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+  const int tab_len = keytab_stride - k0;  // >= 1: every split starts inside the table row
+  const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
+  auto copy_ptrs = [&](int u) {
+    const int r = std::min(u * kKT + (lane >> 1), tab_len - 1);
+    dma4(reinterpret_cast<const unsigned char *>(tab + r) + 4 * (lane & 1), lds_p + (u % kPSlots) * (kKT * 8));
+  };
+  if (wv == 4)
+    for (int u = 0; u < 5; ++u) copy_ptrs(u);
+  if (status != TV_ROW_OK || k0 >= n_keys) {
+    vm_wait<0>();  // no copy into LDS outlives the workgroup
+    return;
+  }
   const int nkeys = std::min(n_keys, k0 + chunk) - k0;
   const int T = (nkeys + kKT - 1) / kKT;
   const bool single = n_keys <= chunk;
@@ -140,26 +156,19 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   const int g_lo = wv == 4 ? 0 : wv == 5 ? 3 : wv == 3 ? 6 : wv == 2 ? 8 : 0;
   const int g_hi = wv == 4 ? 3 : wv == 5 ? 6 : wv == 3 ? 8 : wv == 2 ? 9 : 0;
   const int n_g = 4 * (g_hi - g_lo);
-  const uint16_t *const *tab = keytab + node * keytab_stride + k0;
   const uint32_t lds_k = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sK[0][0];
-  const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
-  // Pointer table of tile u (w4 only): lane l copies 4 bytes (half l & 1) of
-  // the pointer of key min(32 u + l / 2, nkeys - 1), so rows past the
-  // split's end repeat its last key (finite data; their probabilities are 0).
-  auto copy_ptrs = [&](int u) {
-    const int r = std::min(u * kKT + (lane >> 1), nkeys - 1);
-    dma4(reinterpret_cast<const unsigned char *>(tab + r) + 4 * (lane & 1), lds_p + (u % kPSlots) * (kKT * 8));
-  };
   // Rows of tile u into buffer u % 4: instruction (g, k) fills rows 8k ..
   // 8k+7 of group g (lane = row-in-8 * 8 + slot); slot s of row r holds
-  // logical chunk slot(r, s) of the group.  All source addresses are formed
-  // before the first copy is issued.
+  // logical chunk slot(r, s) of the group.  Rows past the split's end repeat
+  // its last key (finite data; their probabilities are 0).  All source
+  // addresses are formed before the first copy is issued.
   auto copy_tile = [&](int u) {
     const unsigned char *src[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int r = 8 * k + (lane >> 3);
-      src[k] = reinterpret_cast<const unsigned char *>(sPtr[u % kPSlots][r]) + slot(r, lane & 7) * 16;
+      const int rv = std::min(r, nkeys - 1 - u * kKT);
+      src[k] = reinterpret_cast<const unsigned char *>(sPtr[u % kPSlots][rv]) + slot(r, lane & 7) * 16;
     }
     const uint32_t dst = lds_k + (u % kNBUF) * kTB;
     const unsigned char *a[3][4];
@@ -174,9 +183,10 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
         for (int k = 0; k < 4; ++k) dma16(a[gg][k], dst + (g_lo + gg) * kGB + k * 1024);
   };
   // The copying waves' share of an attempt's prologue and of iteration it.
-  auto copy_prologue = [&]() {
+  auto copy_prologue = [&](int attempt) {
     if (wv == 4) {
-      for (int u = 0; u < std::min(T, 5); ++u) copy_ptrs(u);
+      if (attempt > 0)  // the first attempt's tables went out with the row status
+        for (int u = 0; u < std::min(T, 5); ++u) copy_ptrs(u);
       vm_wait<0>();
     }
     lds_barrier();  // pointer tables of tiles 0..4 copied
@@ -304,7 +314,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   } else if (wv == 4 || wv == 5) {
     // ---- copy wave ------------------------------------------------------------
     for (int attempt = 0;; ++attempt) {
-      copy_prologue();
+      copy_prologue(attempt);
       lds_barrier();  // tile 0 landed
       for (int it = -1; it < T; ++it) {
         const int n = copy_step(it);
@@ -368,7 +378,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) acc_o[t][ct] = f32x16{};
       }
-      copy_prologue();
+      copy_prologue(attempt);
       lds_barrier();  // tile 0 landed
       for (int it = -1; it < T; ++it) {
         const int n = copy_step(it);
