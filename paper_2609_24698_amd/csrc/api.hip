@@ -105,9 +105,13 @@ WsLayout ws_layout(const tv_dims &d) {
   if (w.plan.splits > 1) off = align256(off + sizeof(float) * 2 * nodes * w.plan.splits * d.H);
   w.row_order = off;
   off = align256(off + sizeof(int32_t) * d.B);
+  w.row_rank = off;
+  off = align256(off + sizeof(int32_t) * d.B);
   w.keytab = off;
   off = align256(off + sizeof(void *) * nodes * w.plan.max_keys);
   w.nkeys = off;
+  off = align256(off + sizeof(int32_t) * nodes);
+  w.nkeys_rank = off;
   off = align256(off + sizeof(int32_t) * nodes);
   const int tseg = topk_max_segments(d);
   const int64_t surv = tseg > 1 ? nodes * tseg * d.topk : 0;
@@ -248,19 +252,21 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
   const CacheView cv = view(*cache);
   TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
   int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
+  int32_t *row_rank = reinterpret_cast<int32_t *>(ws + w.row_rank);
   const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
   int32_t *nkeys = reinterpret_cast<int32_t *>(ws + w.nkeys);
+  int32_t *nkeys_rank = reinterpret_cast<int32_t *>(ws + w.nkeys_rank);
   int32_t *surv_idx = reinterpret_cast<int32_t *>(ws + w.surv_idx);
   uint32_t *surv_key = reinterpret_cast<uint32_t *>(ws + w.surv_key);
   int32_t *surv_cnt = reinterpret_cast<int32_t *>(ws + w.surv_cnt);
   TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
-                                       w.score_stride, selp, row_status, row_order, keytab, w.plan.max_keys, nkeys,
-                                       surv_idx, surv_key, surv_cnt, stream));
+                                       w.score_stride, selp, row_status, row_order, row_rank, keytab, w.plan.max_keys,
+                                       nkeys, nkeys_rank, surv_idx, surv_key, surv_cnt, stream));
   if (topk_max_segments(d) > 1)
-    TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, keytab, w.plan.max_keys,
-                                              surv_idx, surv_key, surv_cnt, stream));
-  TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys, w.plan, part_o, part_ml, out, lse,
-                                       stream));
+    TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, row_rank, keytab,
+                                              w.plan.max_keys, surv_idx, surv_key, surv_cnt, stream));
+  TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys_rank, w.plan, part_o, part_ml, out,
+                                       lse, stream));
   if (w.plan.splits > 1)
     TV_LAUNCH("attn_combine", launch_combine(d, row_status, nkeys, w.plan, part_o, part_ml, out, lse, stream));
   return TV_OK;

@@ -82,22 +82,24 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   int i, split;
   const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
   if (rank >= d.B) return;
+  const int64_t rnode = (int64_t)rank * d.D + i;  // key table and key count are kept by (rank, node)
   const int b = row_order[rank];
   const int64_t node = (int64_t)b * d.D + i;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int ht = wv % HT, part = wv / HT;
   const int k0 = split * chunk;
-  // Everything the prologue needs is loaded at once: row status, key count,
-  // this thread's entries of the node's key table (the top-k kernel wrote it;
-  // entries past the count are never used) and the queries.  The table loads
-  // come first so that storing them waits for them only.
-  const int32_t status = row_status[b];
-  const int n_keys = nkeys_tab[node];
+  // Everything the prologue needs is loaded at once: key count (0 for a row
+  // the earlier steps skipped), this thread's entries of the node's key table
+  // (the top-k kernel wrote it; entries past the count are never used) and
+  // the queries.  The table loads come first so that storing them waits for
+  // them only.
+  (void)row_status;
+  const int n_keys = nkeys_tab[rnode];
   constexpr int kPer = (kMaxChunk + NT - 1) / NT;
   const uint16_t *tp[kPer];
   {
-    const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+    const uint16_t *const *tab = keytab + rnode * keytab_stride + k0;
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const int t = tid + NT * u;
@@ -119,7 +121,7 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
       qf[m] = __builtin_bit_cast(bf16x8, v);
     }
   }
-  if (status != TV_ROW_OK || k0 >= n_keys) return;
+  if (k0 >= n_keys) return;
   const int k1 = std::min(n_keys, k0 + chunk);
   const int nkeys = k1 - k0;
   const int ntiles = (nkeys + kKT - 1) / kKT;

@@ -115,19 +115,20 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   int i, split;
   const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
   if (rank >= d.B) return;
+  const int64_t rnode = (int64_t)rank * d.D + i;  // key table and key count are kept by (rank, node)
   const int b = row_order[rank];
   const int64_t node = (int64_t)b * d.D + i;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform role index
   const int l32 = lane & 31, hi = lane >> 5;
   const int k0 = split * chunk;
-  const int32_t status = row_status[b];
-  const int n_keys = nkeys_tab[node];
+  (void)row_status;  // a row the earlier steps skipped has key count 0 here
+  const int n_keys = nkeys_tab[rnode];
   // Pointer table of tile u (w4 only): lane l copies 4 bytes (half l & 1) of
   // the pointer of key 32 u + l / 2, within the node's table row, so it needs
-  // no key count: the tiles 0..4 of the first attempt go out with the row's
-  // status and key count, one round trip earlier.
-  const uint16_t *const *tab = keytab + node * keytab_stride + k0;
+  // no key count: the tiles 0..4 of the first attempt go out with the key
+  // count and the row index, in the workgroup's first round trip.
+  const uint16_t *const *tab = keytab + rnode * keytab_stride + k0;
   const int tab_len = keytab_stride - k0;  // >= 1: every split starts inside the table row
   const uint32_t lds_p = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)&sPtr[0][0];
   auto copy_ptrs = [&](int u) {
@@ -136,7 +137,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   };
   if (wv == 4)
     for (int u = 0; u < 5; ++u) copy_ptrs(u);
-  if (status != TV_ROW_OK || k0 >= n_keys) {
+  if (k0 >= n_keys) {
     vm_wait<0>();  // no copy into LDS outlives the workgroup
     return;
   }

@@ -22,7 +22,8 @@
 //
 // The selecting workgroup also writes its node's key list (one latent-row
 // pointer per key, in attention order) so that the attention kernel starts
-// from a table instead of re-deriving it.
+// from a table instead of re-deriving it; the table and a copy of the key
+// count are kept by (row rank, node), the attention's own order.
 #include <algorithm>
 
 #include "node_keys.h"
@@ -253,9 +254,10 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
                                                      const uint16_t *__restrict__ w_idx,
                                                      const float *__restrict__ scores, int score_stride,
                                                      int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
-                                                     int32_t *__restrict__ row_order,
+                                                     int32_t *__restrict__ row_order, int32_t *__restrict__ row_rank,
                                                      const uint16_t **__restrict__ keytab, int keytab_stride,
-                                                     int32_t *__restrict__ nkeys_tab, int max_seg,
+                                                     int32_t *__restrict__ nkeys_tab, int32_t *__restrict__ nkeys_rank,
+                                                     int max_seg,
                                                      int32_t *__restrict__ surv_idx, uint32_t *__restrict__ surv_key,
                                                      int32_t *__restrict__ surv_cnt) {
   __shared__ SelShared sh;
@@ -280,27 +282,36 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
     qv0 = *reinterpret_cast<const uint4 *>(q_idx + (node * d.H_idx + hl) * 64 + 8 * cc);
     wh0 = bf2f(w_idx[node * d.H_idx + hl]);
   }
-  if (i == 0 && seg == 0) {
-    // Rank of row b by (committed length descending, row ascending), for every
-    // row whatever its status: row_order[rank] = b.
-    int nb = 0;
-    for (int r = tid; r < d.B; r += kTkNT) {
-      const int32_t Lr = c.len[r];
-      nb += (Lr > L || (Lr == L && r < b)) ? 1 : 0;
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) nb += __shfl_xor(nb, o, 64);
-    if (lane == 0) wcnt[wv] = nb;
-    __syncthreads();
-    if (tid == 0) {
-      int rank = 0;
-      for (int w = 0; w < kTkNW; ++w) rank += wcnt[w];
-      row_order[rank] = b;
-    }
+  // Rank of row b by (committed length descending, row ascending), for every
+  // row whatever its status: row_order[rank] = b, row_rank[b] = rank.  The
+  // key table and a copy of the key count are kept by (rank, node), so the
+  // attention reads them from its workgroup index without the row first.
+  // Each wave's count goes to LDS now; the rank is summed after the next
+  // barrier the workgroup passes anyway.
+  int nb = 0;
+  for (int r = tid; r < d.B; r += kTkNT) {
+    const int32_t Lr = c.len[r];
+    nb += (Lr > L || (Lr == L && r < b)) ? 1 : 0;
   }
-  if (status != TV_ROW_OK) return;
-  if (!len_ok(L, d.max_len)) {
-    if (i == 0 && seg == 0 && tid == 0) row_status[b] = TV_ROW_BAD_LEN;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) nb += __shfl_xor(nb, o, 64);
+  if (lane == 0) wcnt[wv] = nb;
+  auto rank_of_row = [&]() {  // after a barrier
+    int rk = 0;
+#pragma unroll
+    for (int w = 0; w < kTkNW; ++w) rk += wcnt[w];
+    if (i == 0 && seg == 0 && tid == 0) {
+      row_order[rk] = b;
+      row_rank[b] = rk;
+    }
+    return rk;
+  };
+  const bool bad_len = !len_ok(L, d.max_len);
+  if (status != TV_ROW_OK || bad_len) {  // the attention skips the node
+    __syncthreads();
+    const int rk = rank_of_row();
+    if (seg == 0 && tid == 0) nkeys_rank[(int64_t)rk * d.D + i] = 0;
+    if (status == TV_ROW_OK && i == 0 && seg == 0 && tid == 0) row_status[b] = TV_ROW_BAD_LEN;
     return;
   }
   const int n4 = L / d.ratio_csa;
@@ -355,7 +366,8 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
       if (lane == 0) scr_score[t] = sum;
     }
   }
-  lds_barrier();  // path, hca_node and the path-entry scores are visible
+  lds_barrier();  // path, hca_node, the path-entry scores and the wave counts of the rank are visible
+  const int64_t rnode = (int64_t)rank_of_row() * d.D + i;
   const int seg_n = cn + nscr;  // path entries follow the committed ones of the last segment
 #pragma unroll
   for (int j = 0; j < kTkKPT; ++j) {
@@ -366,12 +378,15 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
   }
 
   // The node's key table: non-CSA keys here, selected CSA entries below.
-  const uint16_t **tab = keytab + node * keytab_stride;
+  const uint16_t **tab = keytab + rnode * keytab_stride;
   if (seg == 0) {
     for (int t = nk.nsel + tid; t < nk.n_keys; t += kTkNT)
       tab[t] = key_row(d, nk, b, t, nullptr, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128,
                        tree_u);
-    if (tid == 0) nkeys_tab[node] = nk.n_keys;
+    if (tid == 0) {
+      nkeys_tab[node] = nk.n_keys;
+      nkeys_rank[rnode] = nk.n_keys;
+    }
   }
 
   // Select: the taken elements in element order, list[t] (t < taken) in LDS,
@@ -414,6 +429,7 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
                                                            const uint16_t *__restrict__ scr_c4,
                                                            int32_t *__restrict__ sel,
                                                            const int32_t *__restrict__ row_status,
+                                                           const int32_t *__restrict__ row_rank,
                                                            const uint16_t **__restrict__ keytab, int keytab_stride,
                                                            int max_seg, const int32_t *__restrict__ surv_idx,
                                                            const uint32_t *__restrict__ surv_key,
@@ -449,7 +465,7 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   __syncthreads();
   const int total = real_cnt;
   const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  const uint16_t **tab = keytab + node * keytab_stride;
+  const uint16_t **tab = keytab + ((int64_t)row_rank[b] * d.D + i) * keytab_stride;  // kept by (rank, node)
   const int64_t c4b = c.c4_base[b];
   int32_t *out = sel + node * k;
   const bool all = total <= k;  // every real survivor (key above 0) is taken
@@ -479,25 +495,27 @@ bool topk_supported(const tv_dims &d) {
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
-                       int32_t *row_status, int32_t *row_order, const uint16_t **keytab, int32_t keytab_stride,
-                       int32_t *nkeys, int32_t *surv_idx, uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s) {
+                       int32_t *row_status, int32_t *row_order, int32_t *row_rank, const uint16_t **keytab,
+                       int32_t keytab_stride, int32_t *nkeys, int32_t *nkeys_rank, int32_t *surv_idx,
+                       uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s) {
   if (d.D > kMaxScratch || !topk_supported(d)) return hipErrorInvalidValue;
   const int max_seg = topk_max_segments(d);
   topk_kernel<<<(unsigned)((int64_t)d.B * d.D * max_seg), kTkNT, 0, s>>>(
       d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores, score_stride, sel, row_status, row_order,
-      keytab, keytab_stride, nkeys, max_seg, surv_idx, surv_key, surv_cnt);
+      row_rank, keytab, keytab_stride, nkeys, nkeys_rank, max_seg, surv_idx, surv_key, surv_cnt);
   return hipGetLastError();
 }
 
 hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                              const uint16_t *scr_c4, int32_t *sel, const int32_t *row_status,
-                             const uint16_t **keytab, int32_t keytab_stride, const int32_t *surv_idx,
-                             const uint32_t *surv_key, const int32_t *surv_cnt, hipStream_t s) {
+                             const int32_t *row_rank, const uint16_t **keytab, int32_t keytab_stride,
+                             const int32_t *surv_idx, const uint32_t *surv_key, const int32_t *surv_cnt,
+                             hipStream_t s) {
   const int max_seg = topk_max_segments(d);
   if (max_seg <= 1) return hipSuccess;
   topk_merge_kernel<<<(unsigned)((int64_t)d.B * d.D), kTkNT, 0, s>>>(d, c, anc, depth, scr_c4, sel, row_status,
-                                                                     keytab, keytab_stride, max_seg, surv_idx,
-                                                                     surv_key, surv_cnt);
+                                                                     row_rank, keytab, keytab_stride, max_seg,
+                                                                     surv_idx, surv_key, surv_cnt);
   return hipGetLastError();
 }
 

@@ -44,8 +44,10 @@ struct WsLayout {
   size_t part_o;      // float [B*D][splits][H][d_v]
   size_t part_ml;     // float2 [B*D][splits][H] (running max in log2 units, sum)
   size_t row_order;   // int32 [B]: rows by committed length, longest first
-  size_t keytab;      // const uint16_t* [B*D][plan.max_keys]: latent row of every key of every node
+  size_t row_rank;    // int32 [B]: the inverse, rank of every row
+  size_t keytab;      // const uint16_t* [B rank][D][plan.max_keys]: latent row of every key of every node, by rank
   size_t nkeys;       // int32 [B*D]: key count of every node
+  size_t nkeys_rank;  // int32 [B rank][D]: the same counts by rank (0 for a skipped row)
   size_t surv_idx;    // int32 [B*D][topk segments][topk]: survivors of each top-k segment (segmented nodes only)
   size_t surv_key;    // uint32, same shape: their score keys
   size_t surv_cnt;    // int32 [B*D][topk segments]
@@ -68,12 +70,14 @@ hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
-                       int32_t *row_status, int32_t *row_order, const uint16_t **keytab, int32_t keytab_stride,
-                       int32_t *nkeys, int32_t *surv_idx, uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s);
+                       int32_t *row_status, int32_t *row_order, int32_t *row_rank, const uint16_t **keytab,
+                       int32_t keytab_stride, int32_t *nkeys, int32_t *nkeys_rank, int32_t *surv_idx,
+                       uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s);
 hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                              const uint16_t *scr_c4, int32_t *sel, const int32_t *row_status,
-                             const uint16_t **keytab, int32_t keytab_stride, const int32_t *surv_idx,
-                             const uint32_t *surv_key, const int32_t *surv_cnt, hipStream_t s);
+                             const int32_t *row_rank, const uint16_t **keytab, int32_t keytab_stride,
+                             const int32_t *surv_idx, const uint32_t *surv_key, const int32_t *surv_cnt,
+                             hipStream_t s);
 hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_status, const int32_t *row_order,
                        const uint16_t *const *keytab, const int32_t *nkeys, const SplitPlan &plan, float *part_o,
                        float *part_ml, uint16_t *out, float *lse, hipStream_t s);
