@@ -110,7 +110,6 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   __shared__ __attribute__((aligned(16))) const uint16_t *sPtr[kPSlots][kKT];
   __shared__ int sOver[2];
   __shared__ float sSum[kH];
-  __shared__ float sRef[kH];
 
   int i, split;
   const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
@@ -146,9 +145,9 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   const bool single = n_keys <= chunk;
   const float sl2 = d.scale * kLog2e;
   // Every role runs the same barrier sequence per attempt: two in the
-  // prologue, one per iteration but the last, two at the end (E1: loop done;
-  // E2: overflow verdict, sums and references published), and one more before
-  // a restart.  A restart is decided once per attempt, from the largest logit
+  // prologue, one per iteration but the last, one at the end (E: overflow
+  // verdicts and probability sums published, both written right after the
+  // loop), and one more before a restart.  A restart is decided once per attempt, from the largest logit
   // each logit wave saw: any head more than kSlack above its reference.
   auto restart_now = [&](int attempt) { return (sOver[0] | sOver[1]) != 0 && attempt < kMaxRestarts; };
 
@@ -293,12 +292,10 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
         if (it == T - 1) break;
         lds_barrier();
       }
-      lds_barrier();  // E1
       const float seen = fmaxf(m_seen, __shfl_xor(m_seen, 32, 64));
       const bool over = __any(seen > m_ref + kSlack);
       if (lane == 0) sOver[hh] = over ? 1 : 0;
-      if (hi == 0) sRef[head] = m_ref;
-      lds_barrier();  // E2
+      lds_barrier();  // E: the overflow verdicts and the sums are published
       if (!restart_now(attempt)) break;
       m_ref = seen;  // restart from the largest logit seen
       lds_barrier();
@@ -324,8 +321,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
         lds_barrier();
       }
       vm_wait<0>();
-      lds_barrier();  // E1
-      lds_barrier();  // E2
+      lds_barrier();  // E
       if (!restart_now(attempt)) break;
       lds_barrier();
     }
@@ -389,12 +385,11 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
         lds_barrier();
       }
       vm_wait<0>();
-      lds_barrier();  // E1
       if (pq == 0 && hi == 0) {  // every row of the sums' accumulator holds the sum of its lane's head
         sSum[l32] = acc_l[0][0];
         sSum[32 + l32] = acc_l[1][0];
       }
-      lds_barrier();  // E2
+      lds_barrier();  // E
       if (!restart_now(attempt)) break;
       lds_barrier();
     }
