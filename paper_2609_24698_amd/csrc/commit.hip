@@ -7,7 +7,9 @@
 // so they leave no trace in the persistent state.
 //
 // One workgroup per row.  All checks run before the first write, so a failing
-// row is left exactly as it was.
+// row is left exactly as it was.  The row's loads go out together; the copies
+// (ring rows, CSA and HCA entries) form one list of 16-byte chunks whose
+// loads a thread issues before its stores.
 //
 // Refresh schedule (Sec. 4.3): with a designated chain (the root path of
 // primary_last[b]), whose CSA entries the compression already wrote into the
@@ -31,66 +33,96 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
                                                      int32_t *__restrict__ row_status,
                                                      const int32_t *__restrict__ primary_last) {
   __shared__ int32_t path[64];
+  __shared__ int32_t ent[2][64];  // closing path depths: CSA entries to copy, HCA entries
+  __shared__ int nent[2];
   const int b = blockIdx.x, tid = threadIdx.x;
-  if (row_status[b] != TV_ROW_OK) return;
+  const int64_t rb = (int64_t)b * d.D;
+  // every independent load first, one wait for all of them
+  const int32_t status = row_status[b];
   const int32_t L = c.len[b];
+  const int32_t last = accepted_last[b];
+  const int32_t P = primary_last ? primary_last[b] : -1;
+  const int32_t dt = tid < d.D ? depth[rb + tid] : 0;
+  const int32_t cap4 = c.c4_cap[b], cap128 = c.c128_cap[b];
+  const int64_t base4 = c.c4_base[b], base128 = c.c128_base[b];
+  if (status != TV_ROW_OK) return;
   if (!len_ok(L, d.max_len)) {
     if (tid == 0) row_status[b] = TV_ROW_BAD_LEN;
     return;
   }
-  const int32_t last = accepted_last[b];
-  const int32_t P = primary_last ? primary_last[b] : -1;
   if (last < 0 || last >= d.D) {
     if (tid == 0) row_status[b] = TV_ROW_BAD_ACCEPT;
     return;
   }
-  const uint64_t m = anc[(int64_t)b * d.D + last];
-  const uint64_t chain = (P >= 0 && P < d.D) ? anc[(int64_t)b * d.D + P] : 0ull;
-  const int a = depth[(int64_t)b * d.D + last] + 1;
-  if (tid < d.D && ((m >> tid) & 1ull)) path[depth[(int64_t)b * d.D + tid]] = tid;
+  const uint64_t m = anc[rb + last];
+  const uint64_t chain = (P >= 0 && P < d.D) ? anc[rb + P] : 0ull;
+  const int a = depth[rb + last] + 1;
+  if (tid < d.D && ((m >> tid) & 1ull)) path[dt] = tid;
+  if (tid < 2) nent[tid] = 0;
   bool bad = false;
   if (tid < a) {
     const int64_t p = (int64_t)L + tid;  // path node at depth tid stands at L + tid
-    if ((p + 1) % d.ratio_csa == 0 && (p + 1) / d.ratio_csa - 1 >= c.c4_cap[b]) bad = true;
-    if ((p + 1) % d.ratio_hca == 0 && (p + 1) / d.ratio_hca - 1 >= c.c128_cap[b]) bad = true;
+    if ((p + 1) % d.ratio_csa == 0 && (p + 1) / d.ratio_csa - 1 >= cap4) bad = true;
+    if ((p + 1) % d.ratio_hca == 0 && (p + 1) / d.ratio_hca - 1 >= cap128) bad = true;
   }
   if (__syncthreads_or(bad)) {
     if (tid == 0) row_status[b] = TV_ROW_CAPACITY;
     return;
   }
-  const int d_u = d.d_row + d.d_idx;
-  // raw rows -> ring (16-byte chunks)
-  const int cpr = d_u / 8;
-  for (int e = tid; e < a * cpr; e += blockDim.x) {
-    const int t = e / cpr, cc = (e - t * cpr) * 8;
-    const uint4 v = *reinterpret_cast<const uint4 *>(tree_u + ((int64_t)b * d.D + path[t]) * d_u + cc);
-    uint16_t *dst = c.ring + ((int64_t)b * d.ring_cap + ((L + t) & (d.ring_cap - 1))) * d_u + cc;
-    *reinterpret_cast<uint4 *>(dst) = v;
-  }
-  // scratch entries of the closing path nodes -> pools
-  for (int t = 0; t < a; ++t) {
-    const int64_t p = (int64_t)L + t;
-    const int j = path[t];
-    if ((p + 1) % d.ratio_csa == 0 && !((chain >> j) & 1ull)) {
-      const int64_t slot = c.c4_base[b] + (p + 1) / d.ratio_csa - 1;
-      const uint16_t *src = scr_c4 + ((int64_t)b * d.D + j) * d_u;
-      for (int e = tid; e < d_u / 8; e += blockDim.x) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(src + e * 8);
-        if (e * 8 < d.d_row)
-          *reinterpret_cast<uint4 *>(c.c4 + slot * d.d_row + e * 8) = v;
-        else
-          *reinterpret_cast<uint4 *>(c.c4_idx + slot * d.d_idx + (e * 8 - d.d_row)) = v;
-      }
-    }
-    if ((p + 1) % d.ratio_hca == 0) {
-      const int64_t slot = c.c128_base[b] + (p + 1) / d.ratio_hca - 1;
-      const uint16_t *src = scr_c128 + ((int64_t)b * d.D + j) * d.d_row;
-      for (int e = tid; e < d.d_row / 8; e += blockDim.x)
-        *reinterpret_cast<uint4 *>(c.c128 + slot * d.d_row + e * 8) = *reinterpret_cast<const uint4 *>(src + e * 8);
+  // the closing path depths, in depth order (wave 0: ballots over lanes t < a)
+  if (tid < 64) {
+    const int64_t p = (int64_t)L + tid;
+    const bool c4 = tid < a && (p + 1) % d.ratio_csa == 0 && !((chain >> path[tid < a ? tid : 0]) & 1ull);
+    const bool c128 = tid < a && (p + 1) % d.ratio_hca == 0;
+    const uint64_t b4 = __ballot(c4), b128 = __ballot(c128);
+    const uint64_t below = (1ull << tid) - 1ull;  // lanes below this one
+    if (c4) ent[0][__popcll(b4 & below)] = tid;
+    if (c128) ent[1][__popcll(b128 & below)] = tid;
+    if (tid == 0) {
+      nent[0] = __popcll(b4);
+      nent[1] = __popcll(b128);
     }
   }
   __syncthreads();
-  if (tid < d.D) accept_nodes[(int64_t)b * d.D + tid] = tid < a ? path[tid] : -1;
+  // Copies as one list of 16-byte chunks: raw rows of the path into the ring,
+  // CSA entries (latent row, then indexer key) and HCA entries into their
+  // pool slots.  A thread's loads all go out before its stores.
+  const int d_u = d.d_row + d.d_idx;
+  const int cpr = d_u / 8, c4c = d_u / 8, c128c = d.d_row / 8;
+  const int n_ring = a * cpr, n4 = nent[0] * c4c, n128 = nent[1] * c128c;
+  const int total = n_ring + n4 + n128;
+  constexpr int kBatch = 4;
+  for (int e0 = 0; e0 < total; e0 += kBatch * (int)blockDim.x) {
+    uint4 v[kBatch];
+    uint16_t *dst[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int e = e0 + u * (int)blockDim.x + tid;
+      dst[u] = nullptr;
+      v[u] = make_uint4(0, 0, 0, 0);
+      if (e < n_ring) {
+        const int t = e / cpr, cc = (e - t * cpr) * 8;
+        v[u] = *reinterpret_cast<const uint4 *>(tree_u + (rb + path[t]) * d_u + cc);
+        dst[u] = c.ring + ((int64_t)b * d.ring_cap + ((L + t) & (d.ring_cap - 1))) * d_u + cc;
+      } else if (e < n_ring + n4) {
+        const int x = e - n_ring, k = x / c4c, ch = (x - k * c4c) * 8;
+        const int t = ent[0][k];
+        const int64_t slot = base4 + ((int64_t)L + t + 1) / d.ratio_csa - 1;
+        v[u] = *reinterpret_cast<const uint4 *>(scr_c4 + (rb + path[t]) * d_u + ch);
+        dst[u] = ch < d.d_row ? c.c4 + slot * d.d_row + ch : c.c4_idx + slot * d.d_idx + (ch - d.d_row);
+      } else if (e < total) {
+        const int x = e - n_ring - n4, k = x / c128c, ch = (x - k * c128c) * 8;
+        const int t = ent[1][k];
+        const int64_t slot = base128 + ((int64_t)L + t + 1) / d.ratio_hca - 1;
+        v[u] = *reinterpret_cast<const uint4 *>(scr_c128 + (rb + path[t]) * d.d_row + ch);
+        dst[u] = c.c128 + slot * d.d_row + ch;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (dst[u]) *reinterpret_cast<uint4 *>(dst[u]) = v[u];
+  }
+  if (tid < d.D) accept_nodes[rb + tid] = tid < a ? path[tid] : -1;
   if (tid == 0) {
     accept_len[b] = a;
     c.len[b] = L + a;
