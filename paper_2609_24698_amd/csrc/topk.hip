@@ -44,7 +44,7 @@ struct __align__(16) SelShared {
   uint32_t hist[kTkBins];
   int wsum[kTkNW];
   int found[3];
-  int cnt[2][kTopkMergeKPT][kTkNW];  // per slot and wave: keys above the threshold, keys equal to it
+  uint32_t bits[2][16 * kTopkMergeKPT];  // compaction bitmaps in element order: keys above the threshold, equal to it
 };
 
 // Barrier for shared-memory hand-offs only: global loads in flight stay in flight.
@@ -145,80 +145,80 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
 // Ordered compaction of the keys the threshold takes: the element index of
 // the pos-th taken key (in element order) goes to list[pos], pos < k.  The
 // list aliases the histogram, which the threshold search no longer needs.
+// Each wave's ballots of a slot are two words of a bitmap in element order
+// (keys above the threshold, keys equal to it); one scan over the words gives
+// every word the number of taken elements before it (all the keys above,
+// the first `remaining` equal ones), and each thread writes the taken
+// elements of its words.
 template <int KPT>
 __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n, uint32_t prefix, uint32_t pmask,
                                               int remaining, SelShared &sh) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int nr = (n + kTkNT - 1) / kTkNT;
-  // lane j % 64 keeps this wave's counts of slot j (in set j / 64)
-  constexpr int kSets = (KPT + 63) / 64;
-  int my_g[kSets] = {}, my_q[kSets] = {};
+  uint32_t *bg = sh.bits[0], *be = sh.bits[1];
+  // word 16 j + 2 wv + h holds the elements 512 j + 64 wv + 32 h + bit
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     if (j < nr) {
       const uint32_t km = key[j] & pmask;
-      const int g = __popcll(__ballot(km > prefix));
-      const int q = __popcll(__ballot(km == prefix && key[j] != 0u));
-      my_g[j >> 6] = lane == (j & 63) ? g : my_g[j >> 6];
-      my_q[j >> 6] = lane == (j & 63) ? q : my_q[j >> 6];
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kSets; ++u)
-    if (64 * u + lane < KPT) {
-      sh.cnt[0][64 * u + lane][wv] = my_g[u];
-      sh.cnt[1][64 * u + lane][wv] = my_q[u];
-    }
-  lds_barrier();
-  // exclusive prefix over (slot, wave) in element order, by wave 0
-  if (wv == 0) {
-    constexpr int kE = KPT * kTkNW;
-    constexpr int kPer = (kE + 63) / 64;
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      int *base = &sh.cnt[a][0][0];
-      int v[kPer], loc = 0;
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int x = lane * kPer + u;
-        v[u] = x < kE ? base[x] : 0;
-        loc += v[u];
-      }
-      int incl = loc;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += y;
-      }
-      int run = incl - loc;
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int x = lane * kPer + u;
-        if (x < kE) base[x] = run;
-        run += v[u];
+      const uint64_t g = __ballot(km > prefix);
+      const uint64_t q = __ballot(km == prefix && key[j] != 0u);
+      if (lane == 0) {
+        *reinterpret_cast<uint2 *>(&bg[16 * j + 2 * wv]) = make_uint2((uint32_t)g, (uint32_t)(g >> 32));
+        *reinterpret_cast<uint2 *>(&be[16 * j + 2 * wv]) = make_uint2((uint32_t)q, (uint32_t)(q >> 32));
       }
     }
   }
   lds_barrier();
-  // lane j % 64 holds this wave's offsets of slot j; slot j reads them from lane j
+  // thread t takes the words t * per .. t * per + per - 1
+  const int nw = 16 * nr;
+  constexpr int kPerMax = (16 * KPT + kTkNT - 1) / kTkNT;
+  const int per = (nw + kTkNT - 1) / kTkNT;
+  uint32_t wg[kPerMax], wq[kPerMax];
+  uint32_t cnt = 0u;  // above-threshold count | equal count << 16 (each total below 2^16)
 #pragma unroll
-  for (int u = 0; u < kSets; ++u) {
-    my_g[u] = 64 * u + lane < KPT ? sh.cnt[0][64 * u + lane][wv] : 0;
-    my_q[u] = 64 * u + lane < KPT ? sh.cnt[1][64 * u + lane][wv] : 0;
+  for (int u = 0; u < kPerMax; ++u) {
+    const int w = tid * per + u;
+    const bool ok = u < per && w < nw;
+    wg[u] = ok ? bg[w] : 0u;
+    wq[u] = ok ? be[w] : 0u;
+    cnt += (uint32_t)__popc(wg[u]) | ((uint32_t)__popc(wq[u]) << 16);
   }
+  uint32_t incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) sh.wsum[wv] = (int)incl;
+  lds_barrier();
+  uint32_t before = incl - cnt;
+#pragma unroll
+  for (int w = 0; w < kTkNW; ++w) before += w < wv ? (uint32_t)sh.wsum[w] : 0u;
+  int gb = (int)(before & 0xFFFFu), qb = (int)(before >> 16);  // keys above / equal to the threshold before this thread's words
   int32_t *list = reinterpret_cast<int32_t *>(sh.hist);
 #pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    if (j < nr) {
-      const uint32_t km = key[j] & pmask;
-      const bool gt = km > prefix, eq = km == prefix && key[j] != 0u;
-      const uint64_t bg = __ballot(gt), be = __ballot(eq);
-      const int g = __builtin_amdgcn_readlane(my_g[j >> 6], j & 63) +
-                    (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bg >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bg, 0u));
-      const int q = __builtin_amdgcn_readlane(my_q[j >> 6], j & 63) +
-                    (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(be >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)be, 0u));
-      const int pos = gt ? g + std::min(q, remaining) : g + q;
-      if (gt || (eq && q < remaining)) list[pos] = tid + kTkNT * j;
+  for (int u = 0; u < kPerMax; ++u) {
+    const int w = tid * per + u;
+    if (u < per && w < nw) {
+      const int nq = __popc(wq[u]);
+      const int r = std::min(std::max(remaining - qb, 0), nq);  // equal keys of this word that are taken
+      uint32_t eqt = 0u;
+      if (r == nq) {
+        eqt = wq[u];
+      } else if (r > 0) {
+        uint32_t y = wq[u];
+        for (int c = 0; c < r; ++c) y &= y - 1u;  // drop the lowest r
+        eqt = wq[u] ^ y;
+      }
+      uint32_t t = wg[u] | eqt;
+      int pos = gb + std::min(qb, remaining);
+      while (t) {
+        list[pos++] = 32 * w + (__ffs(t) - 1);
+        t &= t - 1u;
+      }
+      gb += __popc(wg[u]);
+      qb += nq;
     }
   }
   lds_barrier();
