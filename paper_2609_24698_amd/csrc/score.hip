@@ -164,6 +164,8 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
                                                        float *__restrict__ scores, int score_stride,
                                                        int chunks_per_row) {
   __shared__ float wsh[64];
+  __shared__ uint4 qtile[64 * 8];
+  __shared__ uint4 ktile[4][32 * 8];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const int b = blockIdx.x / chunks_per_row;
@@ -177,30 +179,56 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
   const int n4 = L / d.ratio_csa;
   const int e0 = ch * kFastChunk + wv * 64;
   if (ch * kFastChunk >= n4) return;
-  // A: query rows 32 t + l32, channels 16 ks + 8 hi (issued with the keys)
-  bf16x8 qa[2][4];
+  // Operands are read as whole 128-byte rows (eight lanes a row, eight rows a
+  // load) and turned into the MFMA layout through LDS: lane l32 + 32 hi holds
+  // channels 16 ks + 8 hi of its row.  In a tile, 16-byte slot c of row r sits
+  // at slot c ^ (r & 7), so the row writes and the column reads are free of
+  // bank conflicts.
+  // A: the tree's 64 (node, head) query rows, loaded once for the workgroup
+  // (wavefront w loads rows 16 w .. 16 w + 15) into a shared tile.
+  uint4 qr[2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int r = t * 32 + l32;
-    const uint4 *src = reinterpret_cast<const uint4 *>(q_idx + ((int64_t)b * M + (r < M ? r : 0)) * 64);
+  for (int u = 0; u < 2; ++u) {
+    const int r = 16 * wv + 8 * u + (lane >> 3);
+    qr[u] = r < M ? reinterpret_cast<const uint4 *>(q_idx + ((int64_t)b * M + r) * 64)[lane & 7]
+                  : make_uint4(0, 0, 0, 0);
+  }
+  // B: the wavefront's 64 keys, through its own 32-row tile in two halves.
+  uint4 kr[8];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint4 v = r < M ? src[ks * 2 + hi] : make_uint4(0, 0, 0, 0);
-      qa[t][ks] = __builtin_bit_cast(bf16x8, v);
-    }
+  for (int u = 0; u < 8; ++u) {
+    const int e = e0 + 8 * u + (lane >> 3);
+    const bool live = e < n4;
+    kr[u] = live ? reinterpret_cast<const uint4 *>(c.c4_idx + (c4b + e) * 64)[lane & 7] : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int r = 16 * wv + 8 * u + (lane >> 3);
+    qtile[r * 8 + ((lane & 7) ^ (r & 7))] = qr[u];
   }
   bf16x8 kb[2][4];
 #pragma unroll
   for (int cc = 0; cc < 2; ++cc) {
-    const int e = e0 + cc * 32 + l32;
-    const bool live = e < n4;
-    const uint4 *ksrc = reinterpret_cast<const uint4 *>(c.c4_idx + (c4b + (live ? e : 0)) * 64);
+    if (cc == 1) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the first half is read out
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = 8 * u + (lane >> 3);
+      ktile[wv][r * 8 + ((lane & 7) ^ (r & 7))] = kr[4 * cc + u];
+    }
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
-      kb[cc][ks] = __builtin_bit_cast(bf16x8, live ? ksrc[ks * 2 + hi] : make_uint4(0, 0, 0, 0));
+      kb[cc][ks] = __builtin_bit_cast(bf16x8, ktile[wv][l32 * 8 + ((2 * ks + hi) ^ (l32 & 7))]);
   }
   if (tid < 64) wsh[tid] = wv_;
   __syncthreads();
+  bf16x8 qa[2][4];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int r = t * 32 + l32;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      qa[t][ks] = __builtin_bit_cast(bf16x8, qtile[r * 8 + ((2 * ks + hi) ^ (r & 7))]);
+  }
 #pragma unroll
   for (int cc = 0; cc < 2; ++cc) {
     const int e = e0 + cc * 32 + l32;

@@ -71,6 +71,20 @@ def test_c3_full_size():
     _full("C3", rows)
 
 
+def test_batch_above_256_rows():
+    """300 ragged rows of the 8-head shape (more rows than one scoring or
+    ranking workgroup has threads): sampled rows on both sides of row 256."""
+    lens = np.random.default_rng(91).integers(520, 3100, size=300).tolist()
+    w = synth.make_workload("C0", seed=91, B=300, lens=lens, max_len_margin=16)
+    rows = [0, 255, 256, 299, int(np.argmax(w.lens))]
+    rows = sorted(set(rows))
+    nodes = [(b, i) for b in rows for i in range(w.D)]
+    _say(f"[workload] C0 B={w.B} D={w.D} rows={rows} lens={[int(w.lens[b]) for b in rows]}")
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
+
+
 def test_c4_full_size():
     """One row of 1M committed tokens: 262,144 indexer candidates per node
     (the global-memory top-k path) and split attention with the combine."""
