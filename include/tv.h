@@ -102,7 +102,8 @@ typedef struct {
   int32_t topk;      /* CSA entries kept per node, 1..8192; with more than 16,896 candidates a node is
                         selected in segments of that many, at most 64 of them and segments x topk <= 34,816
                         (TV_ERR_UNSUPPORTED otherwise) */
-  int32_t ring_cap;  /* raw-token ring slots per row: power of two >= max(window, ratio_csa, ratio_hca) */
+  int32_t ring_cap;  /* raw-token ring slots per row: power of two >= max(window + D, ratio_csa, ratio_hca),
+                        so one commit of up to D rows never writes two rows to one slot */
   int32_t max_len;   /* bound on every len[b]; sizes launches and the verify workspace */
   float scale;       /* logit scale, finite and > 0, normally 1/sqrt(d_k) */
 } tv_dims;

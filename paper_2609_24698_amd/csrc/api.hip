@@ -31,7 +31,11 @@ static tv_status check_dims(const tv_dims *dp) {
   if (d.d_k > d.d_row || d.v_off + d.d_v > d.d_row || d.d_row % 8 || d.d_idx % 8) return TV_ERR_INVALID_ARG;
   if (d.ratio_csa < 1 || d.ratio_hca < 1 || d.ratio_csa > 1024 || d.ratio_hca > 1024) return TV_ERR_INVALID_ARG;
   if (d.window < 1 || d.topk < 1) return TV_ERR_INVALID_ARG;
-  if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window, d.ratio_csa, d.ratio_hca})) return TV_ERR_INVALID_ARG;
+  // The ring must hold the window, a block's committed tail and, on top of
+  // the window, a whole accepted path: a commit of up to D rows then never
+  // writes two of its rows to one slot.
+  if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window + d.D, d.ratio_csa, d.ratio_hca}))
+    return TV_ERR_INVALID_ARG;
   if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
   if (!std::isfinite(d.scale) || !(d.scale > 0.f)) return TV_ERR_INVALID_ARG;
   if (d.B > 4096 || !shape_supported(d) || !topk_supported(d)) return TV_ERR_UNSUPPORTED;
@@ -69,19 +73,27 @@ static tv_status check_device() {
   return verdict[dev] == 1 ? TV_OK : TV_ERR_DEVICE;
 }
 
+// Attention workgroups the split plan aims for, and the fewest keys a split
+// takes when splitting is optional.  Every split pays a prologue (key table,
+// first tiles, queries), an epilogue and a partial-output round trip through
+// memory, so nodes are split only while there are fewer workgroups than
+// compute units to fill.
+#ifndef TV_ATTN_TARGET_WG
+#define TV_ATTN_TARGET_WG 256
+#endif
+#ifndef TV_ATTN_MIN_CHUNK
+#define TV_ATTN_MIN_CHUNK 256
+#endif
+
 SplitPlan split_plan(const tv_dims &d) {
   SplitPlan p;
   const int64_t mk = (int64_t)d.topk + d.max_len / d.ratio_hca + d.D + d.window;
   p.max_keys = (int32_t)mk;
   const int64_t nodes = (int64_t)d.B * d.D;
-  // Splits only until about 128 workgroups exist: every split pays the
-  // prologue (queries, key table, first tiles) and a partial-output round trip
-  // through memory, which measured costlier than idle compute units (a target
-  // of 128 beat 32..2048 on the B=8 and B=32 workloads and the 1M-token row).
-  int splits = (int)std::min<int64_t>(64, std::max<int64_t>(1, (128 + nodes - 1) / nodes));
-  splits = (int)std::min<int64_t>(splits, (mk + 31) / 32);
-  splits = (int)std::max<int64_t>(splits, (mk + kAttnMaxChunk - 1) / kAttnMaxChunk);  // pointer table bound
-  int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
+  int64_t splits = std::max<int64_t>(1, (TV_ATTN_TARGET_WG + nodes - 1) / nodes);
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, mk / TV_ATTN_MIN_CHUNK));
+  splits = std::max<int64_t>(splits, (mk + kAttnMaxChunk - 1) / kAttnMaxChunk);  // pointer table bound
+  const int64_t chunk = ((mk + splits - 1) / splits + 31) / 32 * 32;
   p.chunk = (int32_t)chunk;
   p.splits = (int32_t)((mk + chunk - 1) / chunk);
   return p;
@@ -137,30 +149,31 @@ struct Prof {
   std::vector<hipEvent_t> pool;
   std::vector<ProfRec> recs;
   size_t cap = 0;
-  bool pending = false;
 } g_prof;
 }  // namespace
 
 // Kernels recorded by the round-graph capture running on this thread (-1: none).
 thread_local int t_capture_kernels = -1;
 
-void prof_before(const char *name, hipStream_t s) {
+// Starts the timing of one launch; returns its record index (-1: not timed).
+int prof_before(const char *name, hipStream_t s) {
   if (t_capture_kernels >= 0) {  // inside a graph capture: count, never time
     ++t_capture_kernels;
-    return;
+    return -1;
   }
-  if (!g_prof.on) return;
-  if (g_prof.recs.size() >= g_prof.cap) return;
-  ProfRec r{name, g_prof.pool[2 * g_prof.recs.size()], g_prof.pool[2 * g_prof.recs.size() + 1]};
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.recs.size() >= g_prof.cap) return -1;
+  const int k = (int)g_prof.recs.size();
+  ProfRec r{name, g_prof.pool[2 * k], g_prof.pool[2 * k + 1]};
   hipEventRecord(r.start, s);
   g_prof.recs.push_back(r);
-  g_prof.pending = true;
+  return k;
 }
 
-void prof_after(hipStream_t s) {
-  if (t_capture_kernels >= 0 || !g_prof.on || !g_prof.pending) return;
-  hipEventRecord(g_prof.recs.back().stop, s);
-  g_prof.pending = false;
+void prof_after(int k, hipStream_t s) {
+  if (k < 0) return;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (k < (int)g_prof.recs.size()) hipEventRecord(g_prof.recs[k].stop, s);
 }
 
 static CacheView view(const tv_cache &c) {
@@ -169,9 +182,9 @@ static CacheView view(const tv_cache &c) {
 
 #define TV_LAUNCH(name, call)            \
   do {                                   \
-    prof_before(name, stream);           \
+    const int k_ = prof_before(name, stream); \
     hipError_t e_ = (call);              \
-    prof_after(stream);                  \
+    prof_after(k_, stream);              \
     if (e_ != hipSuccess) return TV_ERR_LAUNCH; \
   } while (0)
 

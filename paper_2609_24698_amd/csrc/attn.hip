@@ -80,7 +80,7 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
   __shared__ float sRef[HT][32];
 
   int i, split;
-  const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
+  const int rank = unit_of(blockIdx.x, d.B, d.D, splits, i, split);
   if (rank >= d.B) return;
   const int64_t rnode = (int64_t)rank * d.D + i;  // key table and key count are kept by (rank, node)
   const int b = row_order[rank];
@@ -521,7 +521,7 @@ static hipError_t launch_attn_t(const tv_dims &d, const uint16_t *q, const int32
                                 const SplitPlan &plan, float *part_o, float *part_ml, uint16_t *out, float *lse,
                                 hipStream_t s) {
   if (plan.chunk > kMaxChunk) return hipErrorInvalidValue;
-  const int64_t grid = (int64_t)((d.B + 7) / 8) * 8 * d.D * plan.splits;
+  const int64_t grid = attn_grid(d, plan);
   attn_kernel<NW, HT, DK, DV, VOFF, DROW><<<dim3((unsigned)grid), NW * 64, 0, s>>>(
       d, q, row_status, row_order, keytab, plan.max_keys, nkeys, plan.chunk, plan.splits, part_o, part_ml, out, lse);
   return hipGetLastError();

@@ -18,12 +18,30 @@ typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 // Decode the XCD-aware block index.  Workgroups are dealt to the 8 XCDs
-// round-robin and each XCD starts its workgroups in order, so rows are dealt
-// to XCDs in the order row_order gives (longest first): every unit of the
-// row of rank rho runs on XCD rho % 8, where the row's shared HCA, window and
-// overlapping CSA entries stay in one L2, and each XCD starts its longest
-// rows first.  Returns the rank; b is valid when the rank is below B.
-__device__ __forceinline__ int unit_of(int blk, int D, int splits, int &i, int &s) {
+// round-robin (XCD = blockIdx % 8) and each XCD starts its workgroups in
+// order.
+//
+// With 8 rows or more, rows are dealt to XCDs in the order row_order gives
+// (longest first): every unit of the row of rank rho runs on XCD rho % 8,
+// where the row's shared HCA, window and overlapping CSA entries stay in one
+// L2, and each XCD starts its longest rows first.
+//
+// With fewer rows that would leave XCDs idle, so the (row, node, split) units
+// are dealt over all eight: consecutive units go to consecutive XCDs.  When a
+// node has 8 splits or more, its split count is padded to a multiple of 8 so
+// that split s of every node runs on XCD s % 8: split s covers the same key
+// positions in every node's list, which past the CSA selections are the same
+// HCA entries, so those stay in one L2.  Padding units return at once.
+//
+// Returns the rank; the unit is valid when the rank is below B.
+__device__ __forceinline__ int unit_of(int blk, int B, int D, int splits, int &i, int &s) {
+  if (B < 8) {
+    const int sp = attn_padded_splits(B, splits);
+    s = blk % sp;
+    const int r = blk / sp;
+    i = r % D;
+    return s < splits ? r / D : B;
+  }
   const int x = blk & 7, q = blk >> 3;
   s = q % splits;
   const int r = q / splits;

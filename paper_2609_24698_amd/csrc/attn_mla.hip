@@ -112,7 +112,7 @@ attn_mla_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__rest
   __shared__ float sSum[kH];
 
   int i, split;
-  const int rank = unit_of(blockIdx.x, d.D, splits, i, split);
+  const int rank = unit_of(blockIdx.x, d.B, d.D, splits, i, split);
   if (rank >= d.B) return;
   const int64_t rnode = (int64_t)rank * d.D + i;  // key table and key count are kept by (rank, node)
   const int b = row_order[rank];
@@ -444,7 +444,7 @@ hipError_t launch_attn_mla(const tv_dims &d, const uint16_t *q, const int32_t *r
   if (plan.chunk > kMaxChunk || d.H != mla::kH || d.d_k != mla::kDK || d.d_v != mla::kDV || d.v_off != 0 ||
       d.d_row != mla::kDK)
     return hipErrorInvalidValue;
-  const int64_t grid = (int64_t)((d.B + 7) / 8) * 8 * d.D * plan.splits;
+  const int64_t grid = attn_grid(d, plan);
   attn_mla_kernel<<<dim3((unsigned)grid), mla::kNT, 0, s>>>(d, q, row_status, row_order, keytab, plan.max_keys, nkeys,
                                                            plan.chunk, plan.splits, part_o, part_ml, out, lse);
   return hipGetLastError();

@@ -57,6 +57,17 @@ struct WsLayout {
 };
 
 SplitPlan split_plan(const tv_dims &d);
+
+// Splits per node as the attention grid lays them out: with fewer than 8
+// rows and 8 splits or more, padded to a multiple of 8 (split s on XCD s % 8).
+__host__ __device__ inline int attn_padded_splits(int B, int splits) {
+  return (B < 8 && splits >= 8) ? (splits + 7) & ~7 : splits;
+}
+// Workgroups of the attention grid (see unit_of).
+inline int64_t attn_grid(const tv_dims &d, const SplitPlan &p) {
+  if (d.B < 8) return (int64_t)d.B * d.D * attn_padded_splits(d.B, p.splits);
+  return (int64_t)((d.B + 7) / 8) * 8 * d.D * p.splits;
+}
 WsLayout ws_layout(const tv_dims &d);
 
 hipError_t launch_mask(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
@@ -99,7 +110,7 @@ hipError_t launch_select(const tv_dims &d, const int32_t *parents, const uint64_
                          int32_t *target, int32_t *accepted_last, int32_t *next_token, hipStream_t s);
 
 // Kernel timing hooks (no-ops unless profiling is enabled).
-void prof_before(const char *name, hipStream_t s);
-void prof_after(hipStream_t s);
+int prof_before(const char *name, hipStream_t s);
+void prof_after(int record, hipStream_t s);
 
 }  // namespace tv

@@ -125,8 +125,13 @@ def _draw_lens(rng, B, spec):
         assert v.shape == (B,)
         return v, np.zeros(B, dtype=np.int64)
     if kind == "loguniform_tail":
+        # Stratified log-uniform draw: row b takes one point of its own 1/B
+        # quantile band (the bands dealt to rows in a random order), so the
+        # batch follows the distribution closely (mean ~15.5K for [1K, 64K])
+        # instead of depending on how B independent draws happen to fall.
         lo, hi = spec[1], spec[2]
-        u = rng.uniform(math.log(lo), math.log(hi), size=B)
+        band = rng.permutation(B)
+        u = math.log(lo) + (band + rng.random(size=B)) / B * (math.log(hi) - math.log(lo))
         base = np.floor(np.exp(u)).astype(np.int64)
         off = rng.integers(1, 128, size=B)  # tail offset in 1..127
         # The first eight rows sit 127-(b mod 4) tokens into a 128-block, so a

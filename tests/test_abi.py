@@ -33,7 +33,10 @@ def _dims(**over):
     return binding.make_dims(d)
 
 
+# ring_cap must be a power of two holding the window plus a whole accepted path (window + D): with window 16 and
+# D 64 a commit of 64 rows into a 32-slot ring would write two rows to one slot.
 BAD = [dict(B=0), dict(D=0), dict(D=65), dict(topk=0), dict(window=0), dict(ring_cap=200), dict(ring_cap=64),
+       dict(ring_cap=128), dict(window=16, D=64, ring_cap=32), dict(window=16, D=64, ring_cap=64),
        dict(ratio_csa=0), dict(max_len=-1), dict(v_off=200), dict(scale=float("inf")),
        dict(scale=0.0), dict(scale=-0.5)]
 

@@ -197,13 +197,15 @@ def test_round_on_own_scratch():
     torch.cuda.synchronize()
     d = w.dims
     nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
-    n4_rows = [int(L) // d["ratio_csa"] for L in w.lens]
+    g4, g128 = r.host("scr_c4"), r.host("scr_c128")
+
+    def own_ref(b, i):
+        return O.verify_node(w, b, i, ref["anc"], ref["depth"], g4, g128)
 
     def rerun_own(b, i, chosen):
-        g4, g128 = r.host("scr_c4"), r.host("scr_c128")
         return O.verify_node(w, b, i, ref["anc"], ref["depth"], g4, g128, chosen=chosen)
 
-    stats = compare_verify(r.host("out"), r.host("lse"), r.host("sel"), ref, nodes, d, n4_rows=n4_rows,
+    stats = compare_verify(r.host("out"), r.host("lse"), r.host("sel"), ref, nodes, d, own_ref=own_ref,
                            rerun=rerun_own)
     _say(f"  own scratch: {stats}")
     com = ref["commit"]
@@ -216,3 +218,48 @@ def test_round_on_own_scratch():
         diff = np.any(g != o, axis=-1)
         if diff.any():  # only entries the path closed, within the bfloat16 tolerance
             assert_bf16_close(g[diff], O.bf16_to_f64(o[diff]), f"committed {name} entries")
+
+
+def test_c3_alt_shape_full_size():
+    """The alternative reading of "shapes as config 1" on the ragged B=64
+    workload: 8 query heads over one 128-wide key and value head, top-k 512,
+    in the benchmark's length bound."""
+    w = bench.bench_workload("C3", 20, 5, shape="mha128")
+    order = np.argsort(w.lens)
+    rows = sorted(set(int(b) for b in [order[-1], order[0], 0, 1, 2, 33]))
+    nodes = [(b, i) for b in rows for i in range(w.D)]
+    _say(f"[workload] C3 alt shape H={w.dims['H']} rows={rows} lens={[int(w.lens[b]) for b in rows]}")
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
+
+
+def test_nullable_outputs():
+    """sel and lse may be NULL (the selection then lives in the workspace) and
+    next_token may be NULL: the outputs that are given equal, bit for bit,
+    those of a call with every output given, and the buffers not passed stay
+    untouched."""
+    w = _small(seed=77)
+    full, bare = _device(w), _device(w)
+    for r in (full, bare):
+        r.mask()
+        r.compress()
+    full.verify()
+    bare.verify(with_sel=False, with_lse=False)
+    torch.cuda.synchronize()
+    assert np.array_equal(bare.host("out"), full.host("out"))
+    assert np.all(bare.host("sel") == -2) and np.all(np.isnan(bare.host("lse")))
+    ref = O.run_round(w)
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    compare_verify(full.host("out"), full.host("lse"), full.host("sel"), ref, nodes, w.dims, rerun=_rerun(w, ref))
+    sel = synth.make_selection(w, vocab=5000)
+    tgt, acc, nxt = O.select_accepted_path(w.parents, sel.draft_tokens, sel.target_logits, ref["status_verify"])
+    for r in (full, bare):
+        r.attach_selection(sel)
+    full.select()
+    bare.select(with_next=False)
+    torch.cuda.synchronize()
+    for r in (full, bare):
+        assert np.array_equal(r.host("target_tokens"), tgt) and np.array_equal(r.host("accepted_last"), acc)
+    assert np.array_equal(full.host("next_token"), nxt)
+    assert np.all(bare.host("next_token") == -2)
