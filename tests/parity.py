@@ -9,6 +9,8 @@ of each other (near ties that float32 scoring may order differently).
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 from oracle import tv_oracle as O
@@ -16,7 +18,13 @@ from oracle import tv_oracle as O
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 TIE_REL = 1e-5
-LSE_ABS = 2e-3
+# lse: the paper and the contract fix no tolerance, so it follows from the
+# kernels' arithmetic.  The value product takes bfloat16 probabilities and the
+# normalising sum is the sum of those same probabilities; bfloat16 has 8 bits
+# of precision, so each probability is off by at most 2^-8 of itself and the
+# sum by at most 2^-8 of itself: |d lse| <= ln(1 + 2^-8) = 3.9e-3 (reached
+# when one key dominates a peaky softmax).  1e-4 covers the float32 logits.
+LSE_ABS = math.log1p(2.0 ** -8) + 1e-4
 
 
 def bf16_err(gpu_bits: np.ndarray, ref_f64: np.ndarray):
