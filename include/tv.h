@@ -182,6 +182,27 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
                               int32_t *row_status, void *workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* Size of the device array tv_verify_attention_noalloc works in. */
+#define TV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* tv_verify_attention without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments (but workspace), same
+ * outputs and errors.  The library allocates nothing either: the workspace is
+ * a static device array of TV_NOALLOC_SCRATCH_BYTES (64 MiB), one per device,
+ * present from the library's first use on a device until the process ends.
+ * Returns TV_ERR_WORKSPACE when tv_verify_workspace_bytes(dims) exceeds it
+ * (it holds the B=64, 64K-token and the 1M-token workloads, 38 and 41 MiB).
+ * Every call on one device shares that device's array: calls that overlap on
+ * one device (on different streams, or from different threads) race on it
+ * and must be serialised by the caller.  Nothing in the array has to start at
+ * zero; its contents on entry are ignored. */
+tv_status tv_verify_attention_noalloc(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                                      const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                                      const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                                      const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel,
+                                      int32_t *row_status, hipStream_t stream);
+
 /* Accepted-path refresh (Sec. 3.2, Sec. 4.2).  The accepted path is the root
  * path of accepted_last[b], a = depth + 1 nodes.  Writes the raw rows of the
  * path into ring slots of positions L..L+a-1, the scratch entry of every path

@@ -21,6 +21,7 @@ ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = range(5)
 
 EXPORTED = (
     "tv_build_tree_mask", "tv_branch_compress", "tv_verify_workspace_bytes", "tv_verify_attention",
+    "tv_verify_attention_noalloc",
     "tv_commit_accepted_path", "tv_select_workspace_bytes", "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_kernels",
     "tv_round_graph_launch", "tv_round_graph_destroy", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
 )
@@ -78,6 +79,7 @@ def lib() -> ctypes.CDLL:
         L.tv_verify_workspace_bytes.argtypes = [dp]
         L.tv_verify_workspace_bytes.restype = sz
         L.tv_verify_attention.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.tv_verify_attention_noalloc.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tv_commit_accepted_path.argtypes = [dp, cp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tv_select_workspace_bytes.argtypes = [dp, i32]
         L.tv_select_workspace_bytes.restype = sz
@@ -92,7 +94,8 @@ def lib() -> ctypes.CDLL:
         L.tv_status_string.restype = ctypes.c_char_p
         L.tv_profile_enable.argtypes = [i32]
         L.tv_profile_read.argtypes = [ctypes.POINTER(TvKernelTime), i32, ctypes.POINTER(i32)]
-        for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_commit_accepted_path",
+        for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_verify_attention_noalloc",
+                     "tv_commit_accepted_path",
                      "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_launch",
                      "tv_round_graph_destroy", "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
             getattr(L, name).restype = ctypes.c_int
@@ -164,6 +167,19 @@ def tv_verify_attention(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4
                                      _ptr(row_status, torch.int32), _ptr(workspace), workspace.numel() *
                                      workspace.element_size(), _stream(stream)),
            "tv_verify_attention")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TV_NOALLOC_SCRATCH_BYTES
+
+
+def tv_verify_attention_noalloc(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx,
+                                w_idx, out, lse, sel, row_status, stream=None) -> None:
+    _check(lib().tv_verify_attention_noalloc(ctypes.byref(dims), ctypes.byref(cache), _ptr(tree_u),
+                                             _ptr(anc, torch.int64), _ptr(depth, torch.int32), _ptr(scr_c4),
+                                             _ptr(scr_c128), _ptr(q), _ptr(q_idx), _ptr(w_idx), _ptr(out),
+                                             _ptr(lse, torch.float32), _ptr(sel, torch.int32),
+                                             _ptr(row_status, torch.int32), _stream(stream)),
+           "tv_verify_attention_noalloc")
 
 
 def tv_commit_accepted_path(dims: TvDims, cache: TvCache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
@@ -281,6 +297,14 @@ class DeviceRound:
         tv_verify_attention(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"], t["scr_c128"],
                             t["q"], t["q_idx"], t["w_idx"], t["out"], t["lse"] if with_lse else None,
                             t["sel"] if with_sel else None, t["row_status"], t["workspace"], stream)
+
+    def verify_noalloc(self, stream=None, with_sel: bool = True, with_lse: bool = True):
+        """verify() through the entry point that takes no workspace."""
+        t = self.t
+        tv_verify_attention_noalloc(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"],
+                                    t["scr_c128"], t["q"], t["q_idx"], t["w_idx"], t["out"],
+                                    t["lse"] if with_lse else None, t["sel"] if with_sel else None,
+                                    t["row_status"], stream)
 
     def commit(self, stream=None):
         t = self.t

@@ -192,6 +192,81 @@ static CacheView view(const tv_cache &c) {
 
 using namespace tv;
 
+// Workspace of tv_verify_attention_noalloc: one array per device, loaded with
+// the library's code object and held until the process ends.  Host code must
+// never pass the array's name to a kernel (on the host it is a stand-in, not
+// a device address): its device address is looked up once per device and
+// cached below.
+static __device__ __align__(256) unsigned char scratch[TV_NOALLOC_SCRATCH_BYTES];
+
+namespace tv {
+
+// Device address of the current device's scratch array (first call on a
+// device: hipGetSymbolAddress with that device current).
+static tv_status noalloc_scratch(void **ptr) {
+  static std::mutex mu;
+  static std::vector<void *> addr;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TV_ERR_DEVICE;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)addr.size() <= dev) addr.resize(dev + 1, nullptr);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TV_ERR_DEVICE;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return TV_OK;
+}
+
+static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                              const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                              const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                              const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel, int32_t *row_status,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
+      !out || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, row_status) ||
+      (lse && !a16(lse)) || (sel && !a16(sel)))
+    return TV_ERR_INVALID_ARG;
+  const WsLayout w = ws_layout(*dims);
+  if (!workspace || workspace_bytes < w.total) return TV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TV_ERR_INVALID_ARG;
+  if ((st = check_device()) != TV_OK) return st;
+  const tv_dims &d = *dims;
+  char *ws = static_cast<char *>(workspace);
+  float *scores = reinterpret_cast<float *>(ws + w.scores);
+  int32_t *selp = sel ? sel : reinterpret_cast<int32_t *>(ws + w.sel);
+  float *part_o = reinterpret_cast<float *>(ws + w.part_o);
+  float *part_ml = reinterpret_cast<float *>(ws + w.part_ml);
+  const CacheView cv = view(*cache);
+  TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
+  int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
+  int32_t *row_rank = reinterpret_cast<int32_t *>(ws + w.row_rank);
+  const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
+  int32_t *nkeys = reinterpret_cast<int32_t *>(ws + w.nkeys);
+  int32_t *nkeys_rank = reinterpret_cast<int32_t *>(ws + w.nkeys_rank);
+  int32_t *surv_idx = reinterpret_cast<int32_t *>(ws + w.surv_idx);
+  uint32_t *surv_key = reinterpret_cast<uint32_t *>(ws + w.surv_key);
+  int32_t *surv_cnt = reinterpret_cast<int32_t *>(ws + w.surv_cnt);
+  TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
+                                       w.score_stride, selp, row_status, row_order, row_rank, keytab, w.plan.max_keys,
+                                       nkeys, nkeys_rank, surv_idx, surv_key, surv_cnt, stream));
+  if (topk_max_segments(d) > 1)
+    TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, row_rank, keytab,
+                                              w.plan.max_keys, surv_idx, surv_key, surv_cnt, stream));
+  TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys_rank, w.plan, part_o, part_ml, out,
+                                       lse, stream));
+  if (w.plan.splits > 1)
+    TV_LAUNCH("attn_combine", launch_combine(d, row_status, nkeys, w.plan, part_o, part_ml, out, lse, stream));
+  return TV_OK;
+}
+
+}  // namespace tv
+
 extern "C" {
 
 const char *tv_status_string(int s) {
@@ -244,45 +319,23 @@ tv_status tv_verify_attention(const tv_dims *dims, const tv_cache *cache, const 
                               const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
                               const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel, int32_t *row_status,
                               void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  return verify_impl(dims, cache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, lse, sel, row_status,
+                     workspace, workspace_bytes, stream);
+}
+
+tv_status tv_verify_attention_noalloc(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                                      const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                                      const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                                      const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel,
+                                      int32_t *row_status, hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
-  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
-      !out || !row_status)
-    return TV_ERR_INVALID_ARG;
-  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, row_status) ||
-      (lse && !a16(lse)) || (sel && !a16(sel)))
-    return TV_ERR_INVALID_ARG;
-  const WsLayout w = ws_layout(*dims);
-  if (!workspace || workspace_bytes < w.total) return TV_ERR_WORKSPACE;
-  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TV_ERR_INVALID_ARG;
+  if (ws_layout(*dims).total > TV_NOALLOC_SCRATCH_BYTES) return TV_ERR_WORKSPACE;
   if ((st = check_device()) != TV_OK) return st;
-  const tv_dims &d = *dims;
-  char *ws = static_cast<char *>(workspace);
-  float *scores = reinterpret_cast<float *>(ws + w.scores);
-  int32_t *selp = sel ? sel : reinterpret_cast<int32_t *>(ws + w.sel);
-  float *part_o = reinterpret_cast<float *>(ws + w.part_o);
-  float *part_ml = reinterpret_cast<float *>(ws + w.part_ml);
-  const CacheView cv = view(*cache);
-  TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
-  int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
-  int32_t *row_rank = reinterpret_cast<int32_t *>(ws + w.row_rank);
-  const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
-  int32_t *nkeys = reinterpret_cast<int32_t *>(ws + w.nkeys);
-  int32_t *nkeys_rank = reinterpret_cast<int32_t *>(ws + w.nkeys_rank);
-  int32_t *surv_idx = reinterpret_cast<int32_t *>(ws + w.surv_idx);
-  uint32_t *surv_key = reinterpret_cast<uint32_t *>(ws + w.surv_key);
-  int32_t *surv_cnt = reinterpret_cast<int32_t *>(ws + w.surv_cnt);
-  TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
-                                       w.score_stride, selp, row_status, row_order, row_rank, keytab, w.plan.max_keys,
-                                       nkeys, nkeys_rank, surv_idx, surv_key, surv_cnt, stream));
-  if (topk_max_segments(d) > 1)
-    TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, row_rank, keytab,
-                                              w.plan.max_keys, surv_idx, surv_key, surv_cnt, stream));
-  TV_LAUNCH("verify_attn", launch_attn(d, q, row_status, row_order, keytab, nkeys_rank, w.plan, part_o, part_ml, out,
-                                       lse, stream));
-  if (w.plan.splits > 1)
-    TV_LAUNCH("attn_combine", launch_combine(d, row_status, nkeys, w.plan, part_o, part_ml, out, lse, stream));
-  return TV_OK;
+  void *ws = nullptr;
+  if ((st = noalloc_scratch(&ws)) != TV_OK) return st;
+  return verify_impl(dims, cache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, lse, sel, row_status,
+                     ws, TV_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const uint16_t *tree_u, const uint64_t *anc,
