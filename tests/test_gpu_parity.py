@@ -114,8 +114,8 @@ SMALL_CASES = [
     dict(name="C1", B=2, D=8, lens=[1000, 3001], seed=40, topk=64),
     dict(name="C1", B=2, D=8, lens=[127, 639], seed=41, topk=512),
     dict(name="C1", B=1, D=8, chain=True, lens=[5119], seed=42, topk=128, scale=8.0 / 24.0),
-    # blocks longer than the compression kernel's one-batch register tile (192 tokens at a 320-wide row, 144 at
-    # 640): the streamed path
+    # compression blocks of 512 and 256 tokens (more rows than the compression kernel's 1024 threads cover in
+    # one pass of its gate-logit loop, 128 tokens) with a larger ring
     dict(name="C0", B=2, D=8, tree="random", lens=[1535, 4090], seed=38, ratio_csa=16, ratio_hca=512, ring_cap=512),
     dict(name="C1", B=2, D=8, lens=[1791, 3327], seed=43, topk=64, ratio_hca=256, ring_cap=256),
 ]
