@@ -12,8 +12,8 @@ The decoder here keeps an explicit growing sequence: it appends one token,
 compresses the block the token closes (if any) into the ratio's entry list,
 and attends as an ordinary decoder over "top-k of all CSA entries so far, all
 HCA entries so far, the last ``window`` tokens".  It never looks at the tree,
-masks, depths or scratch slots, and it has its own bfloat16 rounding written on
-float64 bit fields, so that it also cross-checks the oracle's conversion.
+masks, depths or scratch slots, and it has its own bfloat16 and FP8 E4M3 roundings written on
+float64 bit fields, so that it also cross-checks the oracle's conversions.
 """
 from __future__ import annotations
 
@@ -43,6 +43,51 @@ def _to_bf16(x):
     r = (u + np.uint64((1 << 44) - 1) + keep) & ~np.uint64((1 << 45) - 1)
     y = r.view(np.float64).astype(np.float32)
     return (y.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def _to_e4m3(x):
+    """float64 -> FP8 E4M3 codes (OCP "fn": bias 7, 3 mantissa bits, largest
+    finite 448), rounding to nearest even on float64 bit fields.
+
+    Inputs of magnitude >= 2**-6 give normal results: keep the top 3 of the 52
+    explicit significand bits, round half to even on the 49 discarded bits (a
+    carry may bump the exponent), re-bias the exponent from 1023 to 7, and
+    clamp to 448 (code 0x7E).  Smaller inputs round half to even to a multiple
+    of 2**-9 (possibly 2**-6 itself).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros(x.shape, dtype=np.uint8)
+    for idx, v in np.ndenumerate(x):
+        sign = 0x80 if np.signbit(v) else 0
+        a = abs(float(v))
+        if a < 2.0 ** -6:                                 # multiples of 2**-9 (8 of them is 2**-6, code 0x08)
+            sub = a * 512.0
+            lo = np.floor(sub)
+            frac = sub - lo
+            m = lo + (1.0 if frac > 0.5 or (frac == 0.5 and int(lo) % 2 == 1) else 0.0)
+            out[idx] = sign | int(m)
+            continue
+        u = int(np.float64(a).view(np.uint64))
+        keep = (u >> 49) & 1
+        r = (u + (1 << 48) - 1 + keep) & ~((1 << 49) - 1)
+        exp = ((r >> 52) & 0x7FF) - 1023 + 7
+        man = (r >> 49) & 0x7
+        code = 0x7E if exp > 15 or (exp == 15 and man == 7) else (exp << 3) | man
+        out[idx] = sign | code
+    return out
+
+
+_E4M3_TABLE = np.array([(-1.0 if c & 0x80 else 1.0) * (((c & 7) / 8.0) * 2.0 ** -6 if (c >> 3) & 15 == 0
+                                                      else (1 + (c & 7) / 8.0) * 2.0 ** (((c >> 3) & 15) - 7))
+                        for c in range(256)])
+
+
+def _widen_key(d, bits):
+    """A stored indexer key, widened: bfloat16 bits, or E4M3 codes when the
+    indexer keys are FP8."""
+    if d.get("idx_fmt", 0) == 1:
+        return _E4M3_TABLE[np.asarray(bits, dtype=np.uint8)]
+    return _widen(bits)
 
 
 class LinearState:
@@ -83,7 +128,8 @@ class LinearState:
                 pooled += wgt[t] * block[t]
             bits = _to_bf16(pooled)
             if r == d["ratio_csa"]:
-                self.csa.append((bits[:d["d_row"]], bits[d["d_row"]:]))
+                key = _to_e4m3(pooled[d["d_row"]:]) if d.get("idx_fmt", 0) == 1 else bits[d["d_row"]:]
+                self.csa.append((bits[:d["d_row"]], key))
             else:
                 self.hca.append(bits[:d["d_row"]])
 
@@ -95,7 +141,7 @@ class LinearState:
         w = _widen(w_bits)
         scored = []
         for s, (_, key) in enumerate(self.csa):
-            kk = _widen(key)
+            kk = _widen_key(d, key)
             sc = 0.0
             for h in range(qi.shape[0]):
                 sc += w[h] * max(0.0, float(np.dot(qi[h], kk)))

@@ -51,7 +51,13 @@ The reading taken here (kept identical on the GPU side):
 * one softmax runs over the selected CSA entries, all visible HCA entries and
   the raw window of the last ``window`` positions up to and including the
   node; keys are ``row[:d_k]``, values ``row[v_off:v_off+d_v]``;
-* an entry is visible from the query at its closing position onward.
+* an entry is visible from the query at its closing position onward;
+* with ``dims["idx_fmt"] == 1`` (a fidelity reading of DeepSeek-V4's FP8
+  indexer keys, which the paper does not restate) every stored indexer key
+  holds OCP FP8 E4M3 values: the committed pool ``c4_idx`` as E4M3 codes, a
+  CSA scratch entry's indexer channels as the same values widened to
+  bfloat16.  The pooled key is rounded to E4M3 (nearest, ties to even,
+  saturating at +-448) instead of to bfloat16; scoring widens it exactly.
 
 All arithmetic is float64.  Inputs are bfloat16 bit patterns, widened
 exactly; a value the cache stores (a compressed entry) is rounded to
@@ -96,6 +102,72 @@ def f64_to_bf16(x) -> np.ndarray:
 
 def round_bf16(x) -> np.ndarray:
     return bf16_to_f64(f64_to_bf16(x))
+
+
+# --------------------------------------------------------------------------
+# FP8 E4M3 (OCP "fn" variant: 1 sign, 4 exponent bits with bias 7, 3 mantissa
+# bits; no infinities, codes 0x7F and 0xFF are NaN; largest finite 448)
+# --------------------------------------------------------------------------
+IDX_BF16, IDX_E4M3 = 0, 1
+E4M3_MAX = 448.0
+
+
+def e4m3_to_f64(codes) -> np.ndarray:
+    """E4M3 codes (uint8) to float64, exactly: exponent field 0 holds the
+    subnormals m * 2**-9, field e > 0 the normals (1 + m/8) * 2**(e-7)."""
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    e = (c >> 3) & 0xF
+    m = (c & 0x7).astype(np.float64)
+    mag = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.ldexp(1.0, e - 7))
+    mag = np.where((c & 0x7F) == 0x7F, np.nan, mag)
+    return np.where(c & 0x80, -mag, mag)
+
+
+def f64_to_e4m3(x) -> np.ndarray:
+    """float64 to E4M3 codes, one rounding to nearest with ties to even;
+    magnitudes beyond 448 saturate to +-448.
+
+    E4M3 keeps 4 significant bits, so around ``|x| = f * 2**E`` (0.5 <= f < 1)
+    representable values are ``2**(E-4)`` apart, never closer than the
+    subnormal spacing ``2**-9``.  ``|x| / spacing`` is an exact power-of-two
+    scaling and ``rint`` rounds it half to even; the rounded magnitude is then
+    encoded field by field.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("non-finite value")
+    a = np.abs(x)
+    _, E = np.frexp(a)
+    spacing = np.ldexp(1.0, np.maximum(E - 4, -9))
+    y = np.minimum(np.rint(a / spacing) * spacing, E4M3_MAX)
+    _, Ey = np.frexp(y)                      # y = fy * 2**Ey, 0.5 <= fy < 1 (Ey = 0 for y = 0)
+    normal = y >= 2.0 ** -6
+    e_field = np.where(normal, Ey - 1 + 7, 0)
+    m_field = np.where(normal, np.rint((y / np.ldexp(1.0, Ey - 1) - 1.0) * 8.0), np.rint(y / 2.0 ** -9))
+    code = (e_field.astype(np.int64) << 3) | m_field.astype(np.int64)
+    code = np.where(np.signbit(x), code | 0x80, code)
+    return code.astype(np.uint8)
+
+
+def round_e4m3(x) -> np.ndarray:
+    return e4m3_to_f64(f64_to_e4m3(x))
+
+
+def idx_fmt(dims) -> int:
+    return int(dims.get("idx_fmt", IDX_BF16))
+
+
+def stored_idx_to_f64(dims, bits) -> np.ndarray:
+    """Committed indexer keys of the pool, widened: bfloat16 or E4M3 codes."""
+    return e4m3_to_f64(bits) if idx_fmt(dims) == IDX_E4M3 else bf16_to_f64(bits)
+
+
+def scratch_idx_to_pool(dims, scr_bits) -> np.ndarray:
+    """The pool's form of a scratch entry's indexer channels: the same values,
+    as bfloat16 bits or (exactly) as E4M3 codes."""
+    if idx_fmt(dims) == IDX_E4M3:
+        return f64_to_e4m3(bf16_to_f64(scr_bits))
+    return np.asarray(scr_bits, dtype=np.uint16).copy()
 
 
 # --------------------------------------------------------------------------
@@ -196,6 +268,8 @@ def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None):
                 toks = np.stack([_token(wl, b, path, L, q) for q in range(p - r + 1, p + 1)])
                 e = compress_block(toks, g[ri])
                 if ri == 0:
+                    if idx_fmt(d) == IDX_E4M3:  # the indexer key is stored as E4M3
+                        e = np.concatenate([e[:d_row], round_e4m3(e[d_row:])])
                     scr_c4[b, i] = f64_to_bf16(e)
                     w4[b, i] = True
                 else:
@@ -216,7 +290,7 @@ class _RowCache:
         self.n4 = L // d["ratio_csa"]
         self.n128 = L // d["ratio_hca"]
         base4, base128 = int(wl.c4_base[b]), int(wl.c128_base[b])
-        self.k4 = bf16_to_f64(wl.c4_idx[base4:base4 + self.n4])
+        self.k4 = stored_idx_to_f64(d, wl.c4_idx[base4:base4 + self.n4])
         self.c4_bits = wl.c4[base4:base4 + self.n4]
         self.c128 = bf16_to_f64(wl.c128[base128:base128 + self.n128])
 
@@ -353,7 +427,7 @@ def write_through(wl, anc, depth, scr_c4, w4, primary_last, row_status):
             s = (L + int(depth[b, j]) + 1) // d["ratio_csa"] - 1
             if s < wl.c4_cap[b]:
                 c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
-                c4_idx[wl.c4_base[b] + s] = scr_c4[b, j, d_row:]
+                c4_idx[wl.c4_base[b] + s] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
     return c4, c4_idx
 
 
@@ -412,7 +486,7 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
             if j in skip4:
                 continue
             c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
-            c4_idx[wl.c4_base[b] + s] = scr_c4[b, j, d_row:]
+            c4_idx[wl.c4_base[b] + s] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
         for s, j in writes128:
             c128[wl.c128_base[b] + s] = scr_c128[b, j]
         lens[b] = L + len(path)

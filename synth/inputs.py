@@ -47,6 +47,7 @@ CONFIGS: Dict[str, dict] = {
 }
 
 BF16_NAN = 0x7FC0  # poison for storage the verify path must never read
+E4M3_NAN = 0x7F    # the same poison for FP8 E4M3 indexer-key slots
 
 
 def _f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -54,6 +55,15 @@ def _f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
     bias = np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
     return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def _bf16_bits_to_e4m3(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns -> FP8 E4M3 codes by torch's float8_e4m3fn
+    conversion (the generator's values are far inside the E4M3 range)."""
+    import torch
+
+    f = torch.from_numpy((bits.astype(np.uint32) << np.uint32(16)).view(np.float32))
+    return f.to(torch.float8_e4m3fn).view(torch.uint8).numpy().copy()
 
 
 def _normal_bf16(rng: np.random.Generator, shape, std: float = 1.0, chunk: int = 1 << 24) -> np.ndarray:
@@ -78,7 +88,7 @@ class Workload:
     accepted_last: np.ndarray   # int32 [B], last node of the accepted root path
     ring: np.ndarray            # uint16 [B][ring_cap][d_u], position q in slot q & (ring_cap-1)
     c4: np.ndarray              # uint16 [c4_total][d_row]
-    c4_idx: np.ndarray          # uint16 [c4_total][d_idx]
+    c4_idx: np.ndarray          # [c4_total][d_idx]: uint16 bfloat16, or uint8 FP8 E4M3 codes when idx_fmt is 1
     c128: np.ndarray            # uint16 [c128_total][d_row]
     c4_base: np.ndarray         # int64 [B]
     c4_cap: np.ndarray          # int32 [B]
@@ -109,9 +119,10 @@ def config_dims(name: str, **over) -> dict:
     dims = dict(B=cfg["B"], D=cfg["D"], topk=cfg["topk"])
     dims.update(SHAPES[cfg["shape"]])
     dims.update(_COMMON)
-    for k in ("d_idx", "H_idx", "ratio_csa", "ratio_hca", "window", "ring_cap", "H"):
+    for k in ("d_idx", "H_idx", "ratio_csa", "ratio_hca", "window", "ring_cap", "H", "idx_fmt"):
         if k in over:
             dims[k] = over[k]
+    dims.setdefault("idx_fmt", 0)
     dims["scale"] = float(over.get("scale", 1.0 / math.sqrt(dims["d_k"])))
     return dims
 
@@ -187,7 +198,8 @@ def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
     ``lens`` overrides the committed lengths (an int or a list of B ints);
     ``tree`` overrides the tree shape ("random" or one parent list for every
     row); ``chain=True`` replaces the tree by a chain on identical bytes;
-    ``over`` overrides B, D, topk, shape, H_idx, window, ring_cap, scale.
+    ``over`` overrides B, D, topk, shape, H_idx, window, ring_cap, scale,
+    idx_fmt (1: committed indexer keys as FP8 E4M3 codes).
     ``extra_c4``/``extra_c128`` are the spare pool slots per row that commits
     append into; ``max_len_margin`` is added to the largest length to form the
     ``max_len`` bound that sizes the verify workspace.
@@ -227,12 +239,15 @@ def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
     t4, t128 = int(c4_cap.sum()), int(c128_cap.sum())
 
     c4 = np.full((t4, d_row), BF16_NAN, dtype=np.uint16)
-    c4_idx = np.full((t4, d_idx), BF16_NAN, dtype=np.uint16)
+    fp8 = dims["idx_fmt"] == 1
+    c4_idx = np.full((t4, d_idx), E4M3_NAN if fp8 else BF16_NAN, dtype=np.uint8 if fp8 else np.uint16)
     c128 = np.full((t128, d_row), BF16_NAN, dtype=np.uint16)
     tot4 = int(n4.sum())
     tot128 = int(n128.sum())
     v4 = _normal_bf16(rng, (tot4, d_row))
     v4i = _normal_bf16(rng, (tot4, d_idx))
+    if fp8:  # the same draws, stored as FP8 E4M3 codes (torch's float32 -> e4m3fn conversion)
+        v4i = _bf16_bits_to_e4m3(v4i)
     v128 = _normal_bf16(rng, (tot128, d_row))
     s4 = s128 = 0
     for b in range(B):

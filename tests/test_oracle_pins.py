@@ -60,6 +60,88 @@ def test_bf16_hand_cases():
 
 
 # --------------------------------------------------------------------------
+# FP8 E4M3 (indexer keys, FP8 reading)
+# --------------------------------------------------------------------------
+def test_e4m3_decode_matches_torch_on_every_code():
+    codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = O.e4m3_to_f64(codes)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan) and list(codes[nan]) == [0x7F, 0xFF]
+    assert np.array_equal(got[~nan], ref[~nan]) and np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def test_e4m3_roundtrip_every_finite_code():
+    codes = np.array([c for c in range(256) if c & 0x7F != 0x7F], dtype=np.uint8)
+    assert np.array_equal(O.f64_to_e4m3(O.e4m3_to_f64(codes)), codes)
+
+
+def test_e4m3_matches_torch_within_range():
+    # torch rounds float32 -> e4m3fn once, to nearest even; inside +-464 it agrees
+    # with the saturating reading (beyond, torch gives NaN and the reading +-448)
+    rng = np.random.default_rng(5)
+    x = np.concatenate([rng.standard_normal(100000) * s for s in (1e-3, 0.03, 1.0, 30.0)])
+    x = np.clip(x, -464.0, 464.0).astype(np.float32)
+    mids = O.e4m3_to_f64(np.arange(0, 0x7E, dtype=np.uint8))
+    x = np.concatenate([x, ((mids[:-1] + mids[1:]) / 2).astype(np.float32)])  # every exact midpoint
+    x = np.concatenate([x, -x])
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(O.f64_to_e4m3(x.astype(np.float64)), ref)
+
+
+def test_e4m3_two_independent_roundings_agree():
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal(20000) * np.exp(rng.uniform(-9, 7, 20000))
+    mids = O.e4m3_to_f64(np.arange(0, 0x7E, dtype=np.uint8))
+    x = np.concatenate([x, (mids[:-1] + mids[1:]) / 2, [1e4, -1e4, 448.0, 464.0, 465.0]])
+    assert np.array_equal(O.f64_to_e4m3(x), R._to_e4m3(x))
+
+
+def test_e4m3_hand_cases():
+    # E4M3 spacing just above 1.0 is 2**-3; subnormals are multiples of 2**-9.
+    cases = [
+        (1.0, 0x38),
+        (1.0 + 2 ** -4, 0x38),                   # exact tie, even neighbour is 1.0
+        (1.0 + 3 * 2 ** -4, 0x3A),               # exact tie, even neighbour is 1.25
+        (1.0 + 2 ** -4 + 2 ** -20, 0x39),        # just above the tie
+        (-(1.0 + 2 ** -4 + 2 ** -20), 0xB9),
+        (448.0, 0x7E),                            # largest finite
+        (464.0, 0x7E),                            # tie between 448 and 480 (not finite): even is 448
+        (1e6, 0x7E), (-1e6, 0xFE),                # saturation
+        (2.0 ** -9, 0x01),                        # smallest subnormal
+        (2.0 ** -10, 0x00),                       # tie between 0 and 2**-9: even is 0
+        (3 * 2.0 ** -10, 0x02),                   # tie between 1 and 2 subnormal units: even is 2
+        (7.5 * 2.0 ** -9, 0x08),                  # tie between the largest subnormal and 2**-6: even is 2**-6
+        (0.0, 0x00), (-0.0, 0x80),
+    ]
+    for x, want in cases:
+        assert int(O.f64_to_e4m3(np.array([x]))[0]) == want, x
+
+
+def test_fp8_compressed_key_is_the_e4m3_rounding_of_the_pooled_key():
+    """With FP8 indexer keys a CSA scratch entry keeps its latent channels as
+    bfloat16 and its indexer channels as E4M3 values (held in bfloat16): the
+    compression of a block differs from the bfloat16 reading only there."""
+    w8 = synth.make_workload("C0", lens=2047, idx_fmt=1)
+    w16 = synth.make_workload("C0", lens=2047)
+    d_row = w8.dims["d_row"]
+    assert w8.c4_idx.dtype == np.uint8
+    for w in (w8, w16):
+        w.c4_idx[:] = 0  # committed keys do not enter the compression; align the two workloads
+    r8, r16 = O.run_round(w8), O.run_round(w16)
+    assert r8["w4"].any()
+    a, b = r8["scr_c4"][r8["w4"]], r16["scr_c4"][r16["w4"]]
+    assert np.array_equal(a[:, :d_row], b[:, :d_row])
+    ka, kb = O.bf16_to_f64(a[:, d_row:]), O.bf16_to_f64(b[:, d_row:])
+    assert np.array_equal(O.round_e4m3(ka), ka)  # E4M3 values
+    # both are one rounding of the same pooled value: to E4M3 (spacing 2**(E-3) for |v| in [2**E, 2**(E+1)),
+    # at least 2**-9) and to bfloat16 (spacing 2**(E-7))
+    E = np.floor(np.log2(np.maximum(np.abs(kb), 2.0 ** -6)))
+    assert np.all(np.abs(ka - kb) <= np.maximum(2.0 ** (E - 4), 2.0 ** -10) + 2.0 ** (E - 8))
+    assert np.any(ka != kb)
+
+
+# --------------------------------------------------------------------------
 # verification plan
 # --------------------------------------------------------------------------
 def _read_plans():
@@ -287,6 +369,10 @@ REPLAY_CASES = [
     dict(name="C0", B=2, D=12, tree="random", lens=[126, 1023], seed=35, topk=8, window=16, ring_cap=128),
     dict(name="C1", B=2, D=6, lens=[509, 510], seed=36, topk=24),
     dict(name="C0", B=2, D=6, tree="random", lens=[391, 127], seed=37, topk=12, scale=8.0 / np.sqrt(128)),
+    # FP8 indexer keys
+    dict(name="C0", lens=2047, idx_fmt=1),
+    dict(name="C0", B=3, D=8, tree="random", lens=[381, 382, 383], seed=38, topk=16, idx_fmt=1),
+    dict(name="C1", B=2, D=6, lens=[509, 510], seed=39, topk=24, idx_fmt=1),
 ]
 
 
@@ -331,6 +417,8 @@ def test_commit_equals_linear_replay_state(case):
             assert np.array_equal(com["c128"][b128 + s], st.hca[s])
         # nothing past the new entries was written
         assert np.all(com["c4"][b4 + n4:b4 + w.c4_cap[b]] == synth.inputs.BF16_NAN)
+        idx_nan = synth.inputs.E4M3_NAN if d["idx_fmt"] == 1 else synth.inputs.BF16_NAN
+        assert np.all(com["c4_idx"][b4 + n4:b4 + w.c4_cap[b]] == idx_nan)
         assert np.all(com["c128"][b128 + n128:b128 + w.c128_cap[b]] == synth.inputs.BF16_NAN)
 
 
