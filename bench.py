@@ -67,6 +67,7 @@ NEXT_WORKLOADS = [
     ("C2-chain", "C2", {"chain": True}),
     ("C4", "C4", {}),
     ("C3-8head", "C3", {"shape": "mha128"}),
+    ("C3-fp8keys", "C3", {"idx_fmt": 1}),
 ]
 
 

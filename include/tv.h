@@ -106,7 +106,14 @@ typedef struct {
                         so one commit of up to D rows never writes two rows to one slot */
   int32_t max_len;   /* bound on every len[b]; sizes launches and the verify workspace */
   float scale;       /* logit scale, finite and > 0, normally 1/sqrt(d_k) */
+  int32_t idx_fmt;   /* number format of stored indexer keys: TV_IDX_BF16, or TV_IDX_E4M3 (FP8 keys, a
+                        fidelity reading of the CSA indexer: the c4_idx pool holds one OCP E4M3 code per
+                        channel, and the indexer channels of a CSA scratch entry hold E4M3 values widened
+                        to bfloat16; compression rounds the pooled key to E4M3, nearest even, saturating
+                        at +-448; scoring widens keys exactly and multiplies them with bfloat16 queries) */
 } tv_dims;
+
+enum { TV_IDX_BF16 = 0, TV_IDX_E4M3 = 1 };
 
 /* Committed (persistent) state of every row.  Only tv_commit_accepted_path
  * writes its committed part; verify only reads it (Sec. 4.2: speculative
@@ -117,7 +124,8 @@ typedef struct {
 typedef struct {
   uint16_t *ring;   /* [B][ring_cap][d_row + d_idx]: raw row of position q in slot q & (ring_cap-1) */
   uint16_t *c4;     /* [*][d_row]: CSA entry s of row b at c4[c4_base[b] + s], s < len/ratio_csa */
-  uint16_t *c4_idx; /* [*][d_idx]: indexer key of the same CSA entry */
+  uint16_t *c4_idx; /* [*][d_idx]: indexer key of the same CSA entry (bfloat16 bits, or one byte per
+                       channel, E4M3 codes, with idx_fmt TV_IDX_E4M3) */
   uint16_t *c128;   /* [*][d_row]: HCA entry s of row b at c128[c128_base[b] + s] */
   const int64_t *c4_base;   /* [B] first pool slot of each row */
   const int32_t *c4_cap;    /* [B] pool slots owned by each row */

@@ -230,7 +230,7 @@ def compress_block(tokens, gate):
 # --------------------------------------------------------------------------
 # per-branch compression into scratch
 # --------------------------------------------------------------------------
-def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None):
+def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None, pooled=None):
     """Compressed entries closed by each node along its own branch.
 
     Node i at position ``p = L + depth[i]`` closes a ratio-r block when
@@ -238,7 +238,9 @@ def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None):
     sequence ``committed || root path of i``.  CSA entries (all d_u channels)
     go to ``scr_c4[b][i]``, HCA entries (the d_row latent channels) to
     ``scr_c128[b][i]``; other slots are left as given.  Returns the scratch
-    arrays, the written-slot masks and the updated row status.
+    arrays, the written-slot masks and the updated row status.  A dict given
+    as ``pooled`` receives each entry's value before it is stored (float64),
+    keyed by (b, i, 0 for CSA / 1 for HCA).
     """
     d = wl.dims
     B, D = d["B"], d["D"]
@@ -267,6 +269,8 @@ def branch_compress(wl, anc, depth, row_status, scr_c4=None, scr_c128=None):
                     continue
                 toks = np.stack([_token(wl, b, path, L, q) for q in range(p - r + 1, p + 1)])
                 e = compress_block(toks, g[ri])
+                if pooled is not None:
+                    pooled[(b, i, ri)] = e.copy()
                 if ri == 0:
                     if idx_fmt(d) == IDX_E4M3:  # the indexer key is stored as E4M3
                         e = np.concatenate([e[:d_row], round_e4m3(e[d_row:])])
@@ -554,8 +558,9 @@ def select_accepted_path(parents, draft_tokens, target_logits, row_status):
 def run_round(wl, nodes=None):
     """All four steps on one workload; returns every intermediate."""
     anc, depth, st = build_tree_mask(wl.parents)
-    scr4, scr128, w4, w128, st = branch_compress(wl, anc, depth, st)
+    pooled = {}
+    scr4, scr128, w4, w128, st = branch_compress(wl, anc, depth, st, pooled=pooled)
     out, lse, sel, st_v, det = verify_attention(wl, anc, depth, scr4, scr128, st, nodes)
     com = commit_accepted_path(wl, anc, depth, scr4, scr128, wl.accepted_last, st_v)
-    return dict(anc=anc, depth=depth, scr_c4=scr4, scr_c128=scr128, w4=w4, w128=w128,
+    return dict(anc=anc, depth=depth, scr_c4=scr4, scr_c128=scr128, w4=w4, w128=w128, pooled=pooled,
                 out=out, lse=lse, sel=sel, status_verify=st_v, detail=det, commit=com)

@@ -36,7 +36,7 @@ class TvError(RuntimeError):
 class TvDims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "B", "D", "H", "d_row", "d_k", "v_off", "d_v", "d_idx", "H_idx", "ratio_csa", "ratio_hca", "window",
-        "topk", "ring_cap", "max_len")] + [("scale", ctypes.c_float)]
+        "topk", "ring_cap", "max_len")] + [("scale", ctypes.c_float), ("idx_fmt", ctypes.c_int32)]
 
 
 class TvCache(ctypes.Structure):
@@ -113,6 +113,8 @@ def _check(code: int, where: str) -> None:
 
 
 def make_dims(d: dict) -> TvDims:
+    d = dict(d)
+    d.setdefault("idx_fmt", 0)
     return TvDims(**{f: (float(d[f]) if f == "scale" else int(d[f])) for f, _ in TvDims._fields_})
 
 

@@ -38,6 +38,7 @@ static tv_status check_dims(const tv_dims *dp) {
     return TV_ERR_INVALID_ARG;
   if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
   if (!std::isfinite(d.scale) || !(d.scale > 0.f)) return TV_ERR_INVALID_ARG;
+  if (d.idx_fmt != TV_IDX_BF16 && d.idx_fmt != TV_IDX_E4M3) return TV_ERR_INVALID_ARG;
   if (d.B > 4096 || !shape_supported(d) || !topk_supported(d)) return TV_ERR_UNSUPPORTED;
   return TV_OK;
 }

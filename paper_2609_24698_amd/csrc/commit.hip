@@ -11,6 +11,9 @@
 // (ring rows, CSA and HCA entries) form one list of 16-byte chunks whose
 // loads a thread issues before its stores.
 //
+// With FP8 indexer keys a CSA entry's indexer channels (E4M3 values held
+// in bfloat16 in scratch) are narrowed, exactly, to E4M3 codes in the pool.
+//
 // Refresh schedule (Sec. 4.3): with a designated chain (the root path of
 // primary_last[b]), whose CSA entries the compression already wrote into the
 // pool, the CSA copies of accepted nodes on that chain are skipped: a single
@@ -95,10 +98,12 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
   for (int e0 = 0; e0 < total; e0 += kBatch * (int)blockDim.x) {
     uint4 v[kBatch];
     uint16_t *dst[kBatch];
+    uint8_t *dst8[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int e = e0 + u * (int)blockDim.x + tid;
       dst[u] = nullptr;
+      dst8[u] = nullptr;
       v[u] = make_uint4(0, 0, 0, 0);
       if (e < n_ring) {
         const int t = e / cpr, cc = (e - t * cpr) * 8;
@@ -110,6 +115,10 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
         const int64_t slot = base4 + ((int64_t)L + t + 1) / d.ratio_csa - 1;
         v[u] = *reinterpret_cast<const uint4 *>(scr_c4 + (rb + path[t]) * d_u + ch);
         dst[u] = ch < d.d_row ? c.c4 + slot * d.d_row + ch : c.c4_idx + slot * d.d_idx + (ch - d.d_row);
+        if (ch >= d.d_row && d.idx_fmt == TV_IDX_E4M3) {  // eight E4M3 codes: 8 bytes at byte offset slot*d_idx + ...
+          dst8[u] = reinterpret_cast<uint8_t *>(c.c4_idx) + slot * d.d_idx + (ch - d.d_row);
+          dst[u] = nullptr;
+        }
       } else if (e < total) {
         const int x = e - n_ring - n4, k = x / c128c, ch = (x - k * c128c) * 8;
         const int t = ent[1][k];
@@ -119,8 +128,17 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
       }
     }
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u)
+    for (int u = 0; u < kBatch; ++u) {
       if (dst[u]) *reinterpret_cast<uint4 *>(dst[u]) = v[u];
+      if (dst8[u]) {  // the scratch holds E4M3 values in bfloat16: narrow them exactly
+        uint2 w;
+        w.x = bf16_to_e4m3(v[u].x & 0xFFFF) | (bf16_to_e4m3(v[u].x >> 16) << 8) |
+              (bf16_to_e4m3(v[u].y & 0xFFFF) << 16) | (bf16_to_e4m3(v[u].y >> 16) << 24);
+        w.y = bf16_to_e4m3(v[u].z & 0xFFFF) | (bf16_to_e4m3(v[u].z >> 16) << 8) |
+              (bf16_to_e4m3(v[u].w & 0xFFFF) << 16) | (bf16_to_e4m3(v[u].w >> 16) << 24);
+        *reinterpret_cast<uint2 *>(dst8[u]) = w;
+      }
+    }
   }
   if (tid < d.D) accept_nodes[rb + tid] = tid < a ? path[tid] : -1;
   if (tid == 0) {

@@ -17,6 +17,10 @@
 // chunk) stream them with 16-byte loads, all of a thread's loads in flight
 // together.
 //
+// With FP8 indexer keys the indexer channels of a CSA entry are rounded to
+// E4M3 (held in scratch as the same values in bfloat16, written to a pool
+// slot as E4M3 codes).
+//
 // Refresh schedule (Sec. 4.3): when the caller designates a chain (the root
 // path of primary_last[b]), the CSA entries its nodes close are also written
 // straight into their persistent pool slots.  Those slots lie past the
@@ -218,11 +222,16 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
       float sum = 0.f;
 #pragma unroll
       for (int gg = 0; gg < G; ++gg) sum += part[ri][gg][ch];  // group order
-      const uint16_t v = f2bf(sum);
+      // FP8 indexer keys: the indexer channels of a CSA entry are E4M3 values
+      const bool fp8 = ri == 0 && ch >= d.d_row && d.idx_fmt == TV_IDX_E4M3;
+      const uint32_t code = fp8 ? f32_to_e4m3(sum) : 0u;
+      const uint16_t v = fp8 ? (uint16_t)e4m3_to_bf16(code) : f2bf(sum);
       dst[ch] = v;
       if (ri == 0 && through) {
         if (ch < d.d_row)
           pool_c4[pslot * d.d_row + ch] = v;
+        else if (fp8)
+          reinterpret_cast<uint8_t *>(pool_c4_idx)[pslot * d.d_idx + (ch - d.d_row)] = (uint8_t)code;
         else
           pool_c4_idx[pslot * d.d_idx + (ch - d.d_row)] = v;
       }

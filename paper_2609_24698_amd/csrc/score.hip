@@ -5,6 +5,8 @@
 // tree form the M side of a dense contraction against the row's indexer keys,
 // so the product runs on MFMA (v_mfma_f32_32x32x16_bf16, float32 accumulate);
 // the head reduction runs in a fixed order so scores are bitwise repeatable.
+// FP8 indexer keys (E4M3 codes) are widened exactly to bfloat16 as they are
+// loaded, so the same bfloat16 products score them.
 //
 // General path: a persistent grid strides over the (row, 128-entry chunk)
 // list of all valid rows, so ragged lengths cost no idle workgroups.
@@ -39,6 +41,24 @@ __device__ int block_excl_scan(int v, int *tmp, int *out_excl) {
   return total;
 }
 
+// Eight indexer-key channels (chunk = channel / 8) of pool entry `entry` as
+// loaded: a 16-byte chunk of bfloat16, or with FP8 keys an 8-byte chunk of
+// E4M3 codes (in .x, .y).  key_bf16 widens a loaded chunk to bfloat16; the
+// loads of a thread all go out before any chunk is widened.
+template <bool FP8>
+__device__ __forceinline__ uint4 key_load(const uint16_t *c4_idx, int64_t entry, int chunk) {
+  if (FP8) {
+    const uint2 w = reinterpret_cast<const uint2 *>(reinterpret_cast<const uint8_t *>(c4_idx) + entry * 64)[chunk];
+    return make_uint4(w.x, w.y, 0u, 0u);
+  }
+  return reinterpret_cast<const uint4 *>(c4_idx + entry * 64)[chunk];
+}
+template <bool FP8>
+__device__ __forceinline__ uint4 key_bf16(uint4 v) {
+  return FP8 ? e4m3x8_to_bf16x8(make_uint2(v.x, v.y)) : v;
+}
+
+template <bool FP8>
 __global__ void __launch_bounds__(256) score_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ q_idx,
                                                     const uint16_t *__restrict__ w_idx,
                                                     const int32_t *__restrict__ row_status,
@@ -91,12 +111,13 @@ __global__ void __launch_bounds__(256) score_kernel(tv_dims d, CacheView c, cons
     bf16x8 kb[4];
     {
       const bool live = e < n4;
-      const uint4 *src = reinterpret_cast<const uint4 *>(c.c4_idx + (c.c4_base[b] + (live ? e : 0)) * 64);
+      const int64_t entry = c.c4_base[b] + (live ? e : 0);
+      uint4 raw[4];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        uint4 v = live ? src[ks * 2 + (lane >> 5)] : make_uint4(0, 0, 0, 0);
-        kb[ks] = __builtin_bit_cast(bf16x8, v);
-      }
+      for (int ks = 0; ks < 4; ++ks)
+        raw[ks] = live ? key_load<FP8>(c.c4_idx, entry, ks * 2 + (lane >> 5)) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kb[ks] = __builtin_bit_cast(bf16x8, key_bf16<FP8>(raw[ks]));
     }
     for (int g = 0; g < groups; ++g) {
       f32x16 acc[2];
@@ -158,6 +179,7 @@ __global__ void __launch_bounds__(256) score_kernel(tv_dims d, CacheView c, cons
 // addresses are known, so a chunk costs two memory round trips.
 constexpr int kFastChunk = 256;  // 4 wavefronts x 64 entries
 
+template <bool FP8>
 __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, const uint16_t *__restrict__ q_idx,
                                                        const uint16_t *__restrict__ w_idx,
                                                        const int32_t *__restrict__ row_status,
@@ -194,13 +216,15 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
                   : make_uint4(0, 0, 0, 0);
   }
   // B: the wavefront's 64 keys, through its own 32-row tile in two halves.
+  // Every load is issued (entries past the row re-read its last one, which
+  // exists: n4 > 0 here) and dead lanes are zeroed afterwards, so no branch
+  // separates the loads and all of them are in flight together.
   uint4 kr[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int e = e0 + 8 * u + (lane >> 3);
-    const bool live = e < n4;
-    kr[u] = live ? reinterpret_cast<const uint4 *>(c.c4_idx + (c4b + e) * 64)[lane & 7] : make_uint4(0, 0, 0, 0);
-  }
+  for (int u = 0; u < 8; ++u) kr[u] = key_load<FP8>(c.c4_idx, c4b + std::min(e0 + 8 * u + (lane >> 3), n4 - 1), lane & 7);
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+    if (e0 + 8 * u + (lane >> 3) >= n4) kr[u] = make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int r = 16 * wv + 8 * u + (lane >> 3);
@@ -213,7 +237,7 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int r = 8 * u + (lane >> 3);
-      ktile[wv][r * 8 + ((lane & 7) ^ (r & 7))] = kr[4 * cc + u];
+      ktile[wv][r * 8 + ((lane & 7) ^ (r & 7))] = key_bf16<FP8>(kr[4 * cc + u]);
     }
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
@@ -260,12 +284,18 @@ hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_
     const int chunks = std::max(1, (d.max_len / d.ratio_csa + kFastChunk - 1) / kFastChunk);
     const int64_t grid = (int64_t)d.B * chunks;
     if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
-    score_kernel_h8<<<(unsigned)grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride, chunks);
+    if (d.idx_fmt == TV_IDX_E4M3)
+      score_kernel_h8<true><<<(unsigned)grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride, chunks);
+    else
+      score_kernel_h8<false><<<(unsigned)grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride, chunks);
     return hipGetLastError();
   }
   const int64_t upper = (int64_t)d.B * ((d.max_len / d.ratio_csa + kScoreChunk - 1) / kScoreChunk);
   const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(upper, 2048));
-  score_kernel<<<grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride);
+  if (d.idx_fmt == TV_IDX_E4M3)
+    score_kernel<true><<<grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride);
+  else
+    score_kernel<false><<<grid, 256, 0, s>>>(d, c, q_idx, w_idx, row_status, scores, score_stride);
   return hipGetLastError();
 }
 

@@ -41,6 +41,40 @@ def assert_bf16_close(gpu_bits, ref_f64, what: str):
     return mx, mean
 
 
+# A quantised code (an FP8 E4M3 indexer key) decided from a float32 value on
+# the GPU and a float64 one in the oracle may land on either side of a
+# rounding midpoint the two values straddle: a code one step away is accepted
+# where the oracle's unrounded value lies within this fraction of its
+# magnitude (at least the E4M3 normal threshold 2**-6) of a midpoint.  The
+# GPU's pooled float32 value is off by about 1e-6 of its magnitude.
+E4M3_MID_REL = 1e-4
+
+
+def assert_e4m3_codes(gpu_bf16_bits, ref_pooled_f64, what: str):
+    """FP8 indexer channels of compressed entries (E4M3 values held in
+    bfloat16): codes equal to the oracle's rounding of its pooled value,
+    except one step away at a near-midpoint.  Returns the number of such
+    near-midpoint channels."""
+    g = O.bf16_to_f64(gpu_bf16_bits)
+    assert np.all(np.isfinite(g)), f"{what}: non-finite"
+    gc = O.f64_to_e4m3(g)
+    assert np.array_equal(O.e4m3_to_f64(gc), g), f"{what}: not E4M3 values"
+    rc = O.f64_to_e4m3(ref_pooled_f64)
+    diff = gc != rc
+    if not diff.any():
+        return 0
+    lo, hi = np.minimum(gc, rc)[diff], np.maximum(gc, rc)[diff]
+    v = ref_pooled_f64[diff]
+    va, vb = np.abs(O.e4m3_to_f64(lo)), np.abs(O.e4m3_to_f64(hi))
+    mid = (va + vb) / 2
+    step = (hi & 0x7F).astype(int) - (lo & 0x7F).astype(int)
+    near = np.abs(np.abs(v) - mid) <= E4M3_MID_REL * np.maximum(np.abs(v), 2.0 ** -6)
+    same_sign = (lo & 0x80) == (hi & 0x80)
+    ok = same_sign & (step == 1) & near
+    assert np.all(ok), f"{what}: {int((~ok).sum())} E4M3 codes differ away from a rounding midpoint"
+    return int(diff.sum())
+
+
 def assert_sel_layout(gpu_sel: np.ndarray, n: int, where: str):
     """The ABI's selection layout: the first n entries strictly ascending and
     non-negative, every later slot exactly -1."""

@@ -38,7 +38,7 @@ def _dims(**over):
 BAD = [dict(B=0), dict(D=0), dict(D=65), dict(topk=0), dict(window=0), dict(ring_cap=200), dict(ring_cap=64),
        dict(ring_cap=128), dict(window=16, D=64, ring_cap=32), dict(window=16, D=64, ring_cap=64),
        dict(ratio_csa=0), dict(max_len=-1), dict(v_off=200), dict(scale=float("inf")),
-       dict(scale=0.0), dict(scale=-0.5)]
+       dict(scale=0.0), dict(scale=-0.5), dict(idx_fmt=2), dict(idx_fmt=-1)]
 
 
 @pytest.mark.parametrize("over", BAD, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))

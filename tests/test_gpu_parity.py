@@ -15,7 +15,7 @@ import torch
 import synth
 from oracle import tv_oracle as O
 
-from .parity import assert_bf16_close, compare_verify
+from .parity import assert_bf16_close, assert_e4m3_codes, compare_verify
 
 pytestmark = pytest.mark.gpu
 
@@ -62,7 +62,14 @@ def _check_stages(w, ref, r, nodes=None, rerun=None):
     g4, g128 = r.host("scr_c4"), r.host("scr_c128")
     w4, w128 = ref["w4"], ref["w128"]
     if w4.any():
-        assert_bf16_close(g4[w4], O.bf16_to_f64(ref["scr_c4"][w4]), "scratch CSA entries")
+        if d.get("idx_fmt", 0) == O.IDX_E4M3:  # latent channels bfloat16, indexer channels E4M3 codes
+            d_row = d["d_row"]
+            assert_bf16_close(g4[w4][:, :d_row], O.bf16_to_f64(ref["scr_c4"][w4][:, :d_row]), "scratch CSA entries")
+            pooled = np.stack([ref["pooled"][(b, i, 0)][d_row:] for b, i in zip(*np.nonzero(w4))])
+            near = assert_e4m3_codes(g4[w4][:, d_row:], pooled, "scratch CSA indexer keys")
+            _say(f"  FP8 keys: {int(w4.sum())} entries, {near} near-midpoint codes")
+        else:
+            assert_bf16_close(g4[w4], O.bf16_to_f64(ref["scr_c4"][w4]), "scratch CSA entries")
     if w128.any():
         assert_bf16_close(g128[w128], O.bf16_to_f64(ref["scr_c128"][w128]), "scratch HCA entries")
     assert np.all(g4[~w4] == 0xFFFF) and np.all(g128[~w128] == 0xFFFF), "scratch slot written that closes nothing"
@@ -118,6 +125,11 @@ SMALL_CASES = [
     # one pass of its gate-logit loop, 128 tokens) with a larger ring
     dict(name="C0", B=2, D=8, tree="random", lens=[1535, 4090], seed=38, ratio_csa=16, ratio_hca=512, ring_cap=512),
     dict(name="C1", B=2, D=8, lens=[1791, 3327], seed=43, topk=64, ratio_hca=256, ring_cap=256),
+    # FP8 (E4M3) indexer keys, both scoring kernels (8 indexer heads and D <= 8; the general one)
+    dict(name="C0", lens=2047, idx_fmt=1),
+    dict(name="C0", B=3, D=8, tree="random", lens=[381, 3967, 1023], seed=44, topk=16, idx_fmt=1),
+    dict(name="C1", B=2, D=8, lens=[1000, 3001], seed=45, topk=64, idx_fmt=1),
+    dict(name="C1", B=2, D=12, tree="random", lens=[2043, 5119], seed=46, topk=128, H_idx=4, idx_fmt=1),
 ]
 
 

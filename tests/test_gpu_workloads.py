@@ -186,11 +186,12 @@ def test_indexer_variants(over):
     _check_stages(w, ref, r, rerun=_rerun(w, ref))
 
 
-def test_round_on_own_scratch():
+@pytest.mark.parametrize("idx_fmt", [0, 1], ids=["bf16-keys", "fp8-keys"])
+def test_round_on_own_scratch(idx_fmt):
     """The whole round on the GPU's own intermediates: verify reads the GPU's
     scratch entries (which may differ from the oracle's in the last bit) and
     commit stores them."""
-    w = _small(B=4, lens=(1003, 2047, 1023, 3071), seed=74)
+    w = _small(B=4, lens=(1003, 2047, 1023, 3071), seed=74, idx_fmt=idx_fmt)
     ref = O.run_round(w)
     r = _device(w)
     r.round()
@@ -213,11 +214,29 @@ def test_round_on_own_scratch():
     assert np.array_equal(r.host("ring"), com["ring"])
     assert np.array_equal(r.host("accept_len"), com["accept_len"])
     assert np.array_equal(r.host("accept_nodes"), com["accept_nodes"])
+    # the committed pools are the oracle's commit of the GPU's own scratch, bit for bit
+    own = O.commit_accepted_path(w, ref["anc"], ref["depth"], g4, g128, w.accepted_last, ref["status_verify"])
     for name in ("c4", "c4_idx", "c128"):
+        assert np.array_equal(r.host(name), own[name]), name
+    for name in ("c4", "c128") + (("c4_idx",) if idx_fmt == 0 else ()):
         g, o = r.host(name), com[name]
         diff = np.any(g != o, axis=-1)
         if diff.any():  # only entries the path closed, within the bfloat16 tolerance
             assert_bf16_close(g[diff], O.bf16_to_f64(o[diff]), f"committed {name} entries")
+
+
+def test_c3_fp8_keys_full_size():
+    """The ragged B=64 workload with FP8 (E4M3) indexer keys, in the
+    benchmark's length bound: sampled rows, every closing node's entry."""
+    w = bench.bench_workload("C3", 20, 5, idx_fmt=1)
+    assert w.c4_idx.dtype == np.uint8
+    order = np.argsort(w.lens)
+    rows = sorted(set(int(b) for b in [order[-1], order[0], 0, 1, 2, 3, 21]))
+    nodes = [(b, i) for b in rows for i in range(w.D)]
+    _say(f"[workload] C3 FP8 keys rows={rows} lens={[int(w.lens[b]) for b in rows]}")
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
 
 
 def test_c3_alt_shape_full_size():
