@@ -97,17 +97,31 @@ class LinearState:
         d = wl.dims
         self.d = d
         L = int(wl.lens[b])
-        cap = d["ring_cap"]
-        # raw rows by absolute position (only the recent ones are kept in the ring)
-        self.raw = {}
-        for q in range(max(0, L - cap), L):
-            self.raw[q] = wl.ring[b, q % cap].copy()
         self.L = L
         n4, n128 = L // d["ratio_csa"], L // d["ratio_hca"]
-        b4, b128 = int(wl.c4_base[b]), int(wl.c128_base[b])
-        # CSA entries as (latent row bits, indexer key bits); HCA entries as latent bits
-        self.csa = [(wl.c4[b4 + s].copy(), wl.c4_idx[b4 + s].copy()) for s in range(n4)]
-        self.hca = [wl.c128[b128 + s].copy() for s in range(n128)]
+        self.raw = {}  # raw rows by absolute position (only the recent ones exist)
+        P = d.get("page_size", 0)
+        if P:
+            # paged pool: position q sits in row q % P of physical page table[q // P];
+            # an entry of ratio r is number s % (P / r) of the page holding its first token
+            table = [int(x) for x in wl.page_table[b]]
+            for q in range(max(0, L - max(d["window"], d["ratio_csa"], d["ratio_hca"])), L):
+                self.raw[q] = wl.ring[table[q // P], q % P].copy()
+
+            def slot(s, r):
+                per = P // r
+                return table[s * r // P] * per + s % per
+            self.csa = [(wl.c4[slot(s, d["ratio_csa"])].copy(), wl.c4_idx[slot(s, d["ratio_csa"])].copy())
+                        for s in range(n4)]
+            self.hca = [wl.c128[slot(s, d["ratio_hca"])].copy() for s in range(n128)]
+        else:
+            cap = d["ring_cap"]
+            for q in range(max(0, L - cap), L):
+                self.raw[q] = wl.ring[b, q % cap].copy()
+            b4, b128 = int(wl.c4_base[b]), int(wl.c128_base[b])
+            # CSA entries as (latent row bits, indexer key bits); HCA entries as latent bits
+            self.csa = [(wl.c4[b4 + s].copy(), wl.c4_idx[b4 + s].copy()) for s in range(n4)]
+            self.hca = [wl.c128[b128 + s].copy() for s in range(n128)]
         self.gate = {d["ratio_csa"]: _widen(wl.gate_w[0]), d["ratio_hca"]: _widen(wl.gate_w[1])}
 
     def append(self, token_bits):

@@ -57,7 +57,17 @@ The reading taken here (kept identical on the GPU side):
   holds OCP FP8 E4M3 values: the committed pool ``c4_idx`` as E4M3 codes, a
   CSA scratch entry's indexer channels as the same values widened to
   bfloat16.  The pooled key is rounded to E4M3 (nearest, ties to even,
-  saturating at +-448) instead of to bfloat16; scoring widens it exactly.
+  saturating at +-448) instead of to bfloat16; scoring widens it exactly;
+* with ``dims["page_size"] = P > 0`` (the paged pool of Sec. 4.2: one
+  logical layer of positions viewed as three physical layers that share
+  page-level pointers) a row's positions form logical pages of P tokens and
+  ``page_table[b][j]`` names the physical page of logical page j (-1: not
+  allocated).  That one page id addresses all three layers: the raw rows
+  (``ring`` becomes ``[pages][P][d_u]``, position q at
+  ``[page(q // P)][q % P]``), the CSA entries (``P / ratio_csa`` per page,
+  entry s at slot ``page(s * ratio_csa // P) * (P / ratio_csa) + s % (P /
+  ratio_csa)``) and the HCA entries likewise.  A commit that needs a page
+  the table does not allocate fails the row with CAPACITY.
 
 All arithmetic is float64.  Inputs are bfloat16 bit patterns, widened
 exactly; a value the cache stores (a compressed entry) is rounded to
@@ -212,10 +222,46 @@ def _len_ok(L, dims):
     return 0 <= L <= dims["max_len"]
 
 
+def paged(dims) -> bool:
+    return int(dims.get("page_size", 0)) > 0
+
+
+def _page(wl, b, j):
+    """Physical page of logical page j of row b, or -1 when not allocated."""
+    d = wl.dims
+    return int(wl.page_table[b, j]) if 0 <= j < d["page_stride"] else -1
+
+
+def raw_index(wl, b, q):
+    """Index into ``wl.ring`` of the raw row of position q of row b (None
+    when its page is not allocated): the ring slot q mod ring_cap, or with a
+    paged pool the row's place in its page."""
+    d = wl.dims
+    if not paged(d):
+        return (b, q & (d["ring_cap"] - 1))
+    P = d["page_size"]
+    pg = _page(wl, b, q // P)
+    return None if pg < 0 else (pg, q % P)
+
+
+def pool_index(wl, b, s, layer):
+    """Slot of logical entry s of row b in pool ``layer`` ("c4" for CSA,
+    "c128" for HCA), or None when the row has no slot for it: past its
+    capacity, or with a paged pool in a page the table does not allocate."""
+    d = wl.dims
+    ratio = d["ratio_csa"] if layer == "c4" else d["ratio_hca"]
+    if not paged(d):
+        base, cap = (wl.c4_base, wl.c4_cap) if layer == "c4" else (wl.c128_base, wl.c128_cap)
+        return int(base[b]) + s if s < int(cap[b]) else None
+    per = d["page_size"] // ratio
+    pg = _page(wl, b, s // per)
+    return None if pg < 0 else pg * per + s % per
+
+
 def _token(wl, b, path, L, q):
     """Raw row (float64, all d_u channels) at absolute position q on a branch."""
     if q < L:
-        return bf16_to_f64(wl.ring[b, q & (wl.dims["ring_cap"] - 1)])
+        return bf16_to_f64(wl.ring[raw_index(wl, b, q)])
     return bf16_to_f64(wl.tree_u[b, path[q - L]])
 
 
@@ -293,10 +339,14 @@ class _RowCache:
         self.L = L = int(wl.lens[b])
         self.n4 = L // d["ratio_csa"]
         self.n128 = L // d["ratio_hca"]
-        base4, base128 = int(wl.c4_base[b]), int(wl.c128_base[b])
-        self.k4 = stored_idx_to_f64(d, wl.c4_idx[base4:base4 + self.n4])
-        self.c4_bits = wl.c4[base4:base4 + self.n4]
-        self.c128 = bf16_to_f64(wl.c128[base128:base128 + self.n128])
+        s4 = [pool_index(wl, b, s, "c4") for s in range(self.n4)]
+        s128 = [pool_index(wl, b, s, "c128") for s in range(self.n128)]
+        if None in s4 or None in s128:
+            raise ValueError(f"row {b}: a committed entry has no pool slot")
+        s4, s128 = np.asarray(s4, dtype=np.int64), np.asarray(s128, dtype=np.int64)
+        self.k4 = stored_idx_to_f64(d, wl.c4_idx[s4])
+        self.c4_bits = wl.c4[s4]
+        self.c128 = bf16_to_f64(wl.c128[s128])
 
 
 def indexer_scores(keys, q_idx, w_idx):
@@ -429,9 +479,10 @@ def write_through(wl, anc, depth, scr_c4, w4, primary_last, row_status):
             if not (chain >> j) & 1 or not w4[b, j]:
                 continue
             s = (L + int(depth[b, j]) + 1) // d["ratio_csa"] - 1
-            if s < wl.c4_cap[b]:
-                c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
-                c4_idx[wl.c4_base[b] + s] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
+            slot = pool_index(wl, b, s, "c4")
+            if slot is not None:
+                c4[slot] = scr_c4[b, j, :d_row]
+                c4_idx[slot] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
     return c4, c4_idx
 
 
@@ -440,10 +491,12 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
     """Refresh the committed state along the accepted path of every valid row.
 
     The accepted path is the root path of ``accepted_last[b]`` (a = depth + 1
-    tokens).  Its raw rows enter the ring at positions L..L+a-1, each of its
-    nodes that closed a block writes its scratch entry to the pool at the
-    entry's logical index, and ``len`` becomes L + a.  A row whose new entries
-    would not fit its pool capacity gets status CAPACITY and is left intact.
+    tokens).  Its raw rows enter the ring (or, paged, their pages) at
+    positions L..L+a-1, each of its nodes that closed a block writes its
+    scratch entry to the pool at the entry's logical index, and ``len``
+    becomes L + a.  A row whose new rows or entries would not fit (pool
+    capacity, or a page the table does not allocate) gets status CAPACITY
+    and is left intact.
     With ``primary_last``, CSA entries of accepted nodes on the row's
     designated chain are not copied (``write_through`` put them in place);
     ``pools`` = (c4, c4_idx) then gives the pools as the compression left them.
@@ -451,7 +504,7 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
     """
     d = wl.dims
     B, D = d["B"], d["D"]
-    r4, r128, cap = d["ratio_csa"], d["ratio_hca"], d["ring_cap"]
+    r4, r128 = d["ratio_csa"], d["ratio_hca"]
     d_row = d["d_row"]
     ring, c128 = wl.ring.copy(), wl.c128.copy()
     c4, c4_idx = (wl.c4.copy(), wl.c4_idx.copy()) if pools is None else (pools[0].copy(), pools[1].copy())
@@ -481,18 +534,21 @@ def commit_accepted_path(wl, anc, depth, scr_c4, scr_c128, accepted_last, row_st
                     skip4.add(j)
             if (p + 1) % r128 == 0:
                 writes128.append(((p + 1) // r128 - 1, j))
-        if any(s >= wl.c4_cap[b] for s, _ in writes4) or any(s >= wl.c128_cap[b] for s, _ in writes128):
+        raw_at = [raw_index(wl, b, L + t) for t in range(len(path))]
+        at4 = [pool_index(wl, b, s, "c4") for s, _ in writes4]
+        at128 = [pool_index(wl, b, s, "c128") for s, _ in writes128]
+        if None in raw_at or None in at4 or None in at128:
             status[b] = ROW_CAPACITY
             continue
         for t, j in enumerate(path):
-            ring[b, (L + t) & (cap - 1)] = wl.tree_u[b, j]
-        for s, j in writes4:
+            ring[raw_at[t]] = wl.tree_u[b, j]
+        for (s, j), slot in zip(writes4, at4):
             if j in skip4:
                 continue
-            c4[wl.c4_base[b] + s] = scr_c4[b, j, :d_row]
-            c4_idx[wl.c4_base[b] + s] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
-        for s, j in writes128:
-            c128[wl.c128_base[b] + s] = scr_c128[b, j]
+            c4[slot] = scr_c4[b, j, :d_row]
+            c4_idx[slot] = scratch_idx_to_pool(d, scr_c4[b, j, d_row:])
+        for (s, j), slot in zip(writes128, at128):
+            c128[slot] = scr_c128[b, j]
         lens[b] = L + len(path)
         an[b] = -1
         an[b, :len(path)] = path

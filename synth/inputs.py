@@ -99,6 +99,9 @@ class Workload:
     q_idx: np.ndarray           # uint16 [B][D][H_idx][d_idx]
     w_idx: np.ndarray           # uint16 [B][D][H_idx]
     gate_w: np.ndarray          # uint16 [2][d_u]; row 0 for the CSA ratio, row 1 for the HCA ratio
+    # Paged pool (dims page_size > 0): physical page of each logical page of each row, -1 where not
+    # allocated; ring is then [pages][page_size][d_u] and the pools are laid out page by page.
+    page_table: Optional[np.ndarray] = None
 
     @property
     def B(self) -> int:
@@ -192,7 +195,7 @@ def _draw_accepted(rng, parents):
 
 def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
                   tree=None, lens=None, extra_c4: int = 96, extra_c128: int = 8,
-                  max_len_margin: int = 0, **over) -> Workload:
+                  max_len_margin: int = 0, page_size: int = 0, **over) -> Workload:
     """Draw the workload of configuration ``name`` (C0..C4).
 
     ``lens`` overrides the committed lengths (an int or a list of B ints);
@@ -202,7 +205,8 @@ def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
     idx_fmt (1: committed indexer keys as FP8 E4M3 codes).
     ``extra_c4``/``extra_c128`` are the spare pool slots per row that commits
     append into; ``max_len_margin`` is added to the largest length to form the
-    ``max_len`` bound that sizes the verify workspace.
+    ``max_len`` bound that sizes the verify workspace.  ``page_size`` > 0
+    lays the same state out in a paged pool (see ``paginate``).
     """
     cfg = dict(CONFIGS[name])
     for k in ("B", "D", "topk", "shape"):
@@ -265,13 +269,64 @@ def make_workload(name: str, seed: Optional[int] = None, *, chain: bool = False,
     gate_w = _normal_bf16(rng, (2, d_u), std=0.02)
 
     dims["max_len"] = int(lens_v.max()) + int(max_len_margin)
-    return Workload(
+    dims["page_size"], dims["page_stride"] = 0, 0
+    wl = Workload(
         name=name + ("-chain" if chain else ""), seed=seed, dims=dims,
         lens=lens_v.astype(np.int32), parents=parents, accepted_last=accepted,
         ring=ring, c4=c4, c4_idx=c4_idx, c128=c128,
         c4_base=c4_base, c4_cap=c4_cap, c128_base=c128_base, c128_cap=c128_cap,
         tree_u=tree_u, q=q, q_idx=q_idx, w_idx=w_idx, gate_w=gate_w,
     )
+    return paginate(wl, page_size, seed) if page_size else wl
+
+
+def paginate(wl: Workload, page_size: int, seed: int) -> Workload:
+    """The same logical state in a paged pool of ``page_size``-token pages.
+
+    Each row owns the logical pages covering its CSA capacity (c4_cap *
+    ratio_csa positions); its page-table row has one more entry, left
+    unallocated (-1).  Physical page ids are a random permutation of all
+    owned pages, drawn from a generator of its own so that every other byte
+    equals the flat workload's.  Raw rows of the last ring_cap committed
+    positions are copied from the ring, committed entries from the flat
+    pools; every other slot holds the poison pattern.
+    """
+    d = dict(wl.dims)
+    P = int(page_size)
+    r4, r128, cap = d["ratio_csa"], d["ratio_hca"], d["ring_cap"]
+    assert P % r4 == 0 and P % r128 == 0
+    B = d["B"]
+    owned = [-(-int(wl.c4_cap[b]) * r4 // P) for b in range(B)]
+    stride = max(owned) + 1
+    total = int(sum(owned))
+    perm = np.random.Generator(np.random.PCG64(seed + 104729)).permutation(total).astype(np.int32)
+    table = np.full((B, stride), -1, dtype=np.int32)
+    k = 0
+    for b in range(B):
+        table[b, :owned[b]] = perm[k:k + owned[b]]
+        k += owned[b]
+    d_u = wl.ring.shape[-1]
+    raw = np.full((total, P, d_u), BF16_NAN, dtype=np.uint16)
+    per4, per128 = P // r4, P // r128
+    c4 = np.full((total * per4, wl.c4.shape[1]), BF16_NAN, dtype=np.uint16)
+    c4_idx = np.full((total * per4, wl.c4_idx.shape[1]), E4M3_NAN if wl.c4_idx.dtype == np.uint8 else BF16_NAN,
+                     dtype=wl.c4_idx.dtype)
+    c128 = np.full((total * per128, wl.c128.shape[1]), BF16_NAN, dtype=np.uint16)
+    for b in range(B):
+        L = int(wl.lens[b])
+        for q in range(max(0, L - cap), L):
+            raw[table[b, q // P], q % P] = wl.ring[b, q % cap]
+        n4, n128 = L // r4, L // r128
+        s = np.arange(n4)
+        slots = table[b, s // per4].astype(np.int64) * per4 + s % per4
+        c4[slots] = wl.c4[wl.c4_base[b]:wl.c4_base[b] + n4]
+        c4_idx[slots] = wl.c4_idx[wl.c4_base[b]:wl.c4_base[b] + n4]
+        s = np.arange(n128)
+        slots = table[b, s // per128].astype(np.int64) * per128 + s % per128
+        c128[slots] = wl.c128[wl.c128_base[b]:wl.c128_base[b] + n128]
+    d["page_size"], d["page_stride"] = P, stride
+    return dataclasses.replace(wl, name=wl.name + f"-paged{P}", dims=d, ring=raw, c4=c4, c4_idx=c4_idx,
+                               c128=c128, page_table=table)
 
 
 # DeepSeek-V3's vocabulary size; the paper does not state DeepSeek-V4's, so the
