@@ -68,6 +68,7 @@ NEXT_WORKLOADS = [
     ("C4", "C4", {}),
     ("C3-8head", "C3", {"shape": "mha128"}),
     ("C3-fp8keys", "C3", {"idx_fmt": 1}),
+    ("C3-paged", "C3", {"page_size": 128}),
 ]
 
 

@@ -111,6 +111,10 @@ typedef struct {
                         channel, and the indexer channels of a CSA scratch entry hold E4M3 values widened
                         to bfloat16; compression rounds the pooled key to E4M3, nearest even, saturating
                         at +-448; scoring widens keys exactly and multiplies them with bfloat16 queries) */
+  int32_t page_size;   /* 0: flat pools and a ring per row.  > 0: the paged pool (Sec. 4.2: one logical layer
+                          of positions over three physical layers sharing page-level pointers), pages of
+                          page_size tokens, a power of two and a multiple of ratio_csa and ratio_hca */
+  int32_t page_stride; /* paged pool: page-table entries per row (>= 1) */
 } tv_dims;
 
 enum { TV_IDX_BF16 = 0, TV_IDX_E4M3 = 1 };
@@ -132,6 +136,15 @@ typedef struct {
   const int64_t *c128_base; /* [B] */
   const int32_t *c128_cap;  /* [B] */
   int32_t *len;             /* [B] committed tokens L of each row */
+  /* Paged pool (dims page_size P > 0): page_table [B][page_stride] gives the physical page of each logical
+   * page j (positions jP..jP+P-1) of each row, -1 where none is allocated.  The page id addresses all three
+   * layers: ring becomes [pages][P][d_row + d_idx] (position q at [page(q / P)][q % P]); c4 and c4_idx hold
+   * P/ratio_csa entries per page (entry s at slot page(s * ratio_csa / P) * (P/ratio_csa) + s % (P/ratio_csa)),
+   * c128 likewise with ratio_hca; c4_base, c4_cap, c128_base, c128_cap are not read (may be NULL).  Every
+   * page overlapping positions 0..len-1 must be allocated (compression fails a row whose committed rows it
+   * cannot find, TV_ROW_CAPACITY); a commit needing a page with no id fails the row, TV_ROW_CAPACITY.  Page
+   * ids must lie within the caller's layers.  NULL with page_size 0. */
+  const int32_t *page_table;
 } tv_cache;
 
 /* Verify preprocess (Sec. 4.1): for every row, validate the parent array and

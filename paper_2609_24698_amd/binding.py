@@ -36,12 +36,13 @@ class TvError(RuntimeError):
 class TvDims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "B", "D", "H", "d_row", "d_k", "v_off", "d_v", "d_idx", "H_idx", "ratio_csa", "ratio_hca", "window",
-        "topk", "ring_cap", "max_len")] + [("scale", ctypes.c_float), ("idx_fmt", ctypes.c_int32)]
+        "topk", "ring_cap", "max_len")] + [("scale", ctypes.c_float)] + [(n, ctypes.c_int32) for n in (
+            "idx_fmt", "page_size", "page_stride")]
 
 
 class TvCache(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
-        "ring", "c4", "c4_idx", "c128", "c4_base", "c4_cap", "c128_base", "c128_cap", "len")]
+        "ring", "c4", "c4_idx", "c128", "c4_base", "c4_cap", "c128_base", "c128_cap", "len", "page_table")]
 
 
 class TvLayer(ctypes.Structure):
@@ -114,7 +115,8 @@ def _check(code: int, where: str) -> None:
 
 def make_dims(d: dict) -> TvDims:
     d = dict(d)
-    d.setdefault("idx_fmt", 0)
+    for k in ("idx_fmt", "page_size", "page_stride"):
+        d.setdefault(k, 0)
     return TvDims(**{f: (float(d[f]) if f == "scale" else int(d[f])) for f, _ in TvDims._fields_})
 
 
@@ -135,11 +137,12 @@ def _stream(stream) -> Optional[int]:
     return s.cuda_stream
 
 
-def make_cache(ring, c4, c4_idx, c128, c4_base, c4_cap, c128_base, c128_cap, lens) -> TvCache:
-    """Cache struct over device tensors (bf16/int16 pools, int64 bases, int32 caps and lengths)."""
+def make_cache(ring, c4, c4_idx, c128, c4_base, c4_cap, c128_base, c128_cap, lens, page_table=None) -> TvCache:
+    """Cache struct over device tensors (bf16/int16 pools, int64 bases, int32 caps and lengths; an int32
+    page table for a paged pool)."""
     return TvCache(_ptr(ring), _ptr(c4), _ptr(c4_idx), _ptr(c128), _ptr(c4_base, torch.int64),
                    _ptr(c4_cap, torch.int32), _ptr(c128_base, torch.int64), _ptr(c128_cap, torch.int32),
-                   _ptr(lens, torch.int32))
+                   _ptr(lens, torch.int32), _ptr(page_table, torch.int32))
 
 
 def tv_build_tree_mask(dims: TvDims, parents, anc, depth, row_status, stream=None) -> None:
@@ -258,6 +261,8 @@ class DeviceRound:
                   "c128_cap", "tree_u", "q", "q_idx", "w_idx", "gate_w"):
             T[k] = _dev(getattr(src, k), dev)
         T["len"] = _dev(src.lens.astype(np.int32), dev)
+        pt = getattr(src, "page_table", None)
+        T["page_table"] = _dev(pt.astype(np.int32), dev) if pt is not None else None
         fill = -1 if poison_outputs else 0  # 0xFFFF bf16 is NaN: unwritten outputs show up
         T["anc"] = torch.full((B, D), fill, dtype=torch.int64, device=dev)
         T["depth"] = torch.full((B, D), fill, dtype=torch.int32, device=dev)
@@ -275,7 +280,7 @@ class DeviceRound:
         T["workspace"] = torch.empty(ws, dtype=torch.uint8, device=dev)
         self.t = T
         self.cache = make_cache(T["ring"], T["c4"], T["c4_idx"], T["c128"], T["c4_base"], T["c4_cap"],
-                                T["c128_base"], T["c128_cap"], T["len"])
+                                T["c128_base"], T["c128_cap"], T["len"], T["page_table"])
 
     def mask(self, stream=None):
         t = self.t

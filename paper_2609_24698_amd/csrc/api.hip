@@ -34,8 +34,14 @@ static tv_status check_dims(const tv_dims *dp) {
   // The ring must hold the window, a block's committed tail and, on top of
   // the window, a whole accepted path: a commit of up to D rows then never
   // writes two of its rows to one slot.
-  if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window + d.D, d.ratio_csa, d.ratio_hca}))
+  if (d.page_size < 0 || d.page_stride < 0) return TV_ERR_INVALID_ARG;
+  if (d.page_size > 0) {  // paged pool: pages hold whole CSA and HCA blocks
+    if (!pow2(d.page_size) || d.page_size > (1 << 20) || d.page_size % d.ratio_csa || d.page_size % d.ratio_hca ||
+        d.page_stride < 1)
+      return TV_ERR_INVALID_ARG;
+  } else if (!pow2(d.ring_cap) || d.ring_cap < std::max({d.window + d.D, d.ratio_csa, d.ratio_hca})) {
     return TV_ERR_INVALID_ARG;
+  }
   if (d.max_len < 0 || (int64_t)d.max_len + d.D + 1 >= (int64_t(1) << 30)) return TV_ERR_INVALID_ARG;
   if (!std::isfinite(d.scale) || !(d.scale > 0.f)) return TV_ERR_INVALID_ARG;
   if (d.idx_fmt != TV_IDX_BF16 && d.idx_fmt != TV_IDX_E4M3) return TV_ERR_INVALID_ARG;
@@ -43,9 +49,10 @@ static tv_status check_dims(const tv_dims *dp) {
   return TV_OK;
 }
 
-static bool cache_complete(const tv_cache *c) {
-  return c && c->ring && c->c4 && c->c4_idx && c->c128 && c->c4_base && c->c4_cap && c->c128_base &&
-         c->c128_cap && c->len;
+static bool cache_complete(const tv_dims &d, const tv_cache *c) {
+  if (!c || !c->ring || !c->c4 || !c->c4_idx || !c->c128 || !c->len) return false;
+  if (d.page_size > 0) return c->page_table != nullptr;
+  return c->c4_base && c->c4_cap && c->c128_base && c->c128_cap;
 }
 
 // Kernels move rows with 16-byte loads and stores; every buffer must allow them.
@@ -55,7 +62,9 @@ static bool all_a16(const P *...p) {
   return (a16(p) && ...);
 }
 static bool cache_a16(const tv_cache *c) {
-  return all_a16(c->ring, c->c4, c->c4_idx, c->c128, c->c4_base, c->c4_cap, c->c128_base, c->c128_cap, c->len);
+  auto ok = [](const void *p) { return !p || a16(p); };  // pointers a layout does not use may be NULL
+  return all_a16(c->ring, c->c4, c->c4_idx, c->c128, c->len) && ok(c->c4_base) && ok(c->c4_cap) &&
+         ok(c->c128_base) && ok(c->c128_cap) && ok(c->page_table);
 }
 
 // The library only runs on gfx950; the answer is cached per device.
@@ -178,7 +187,8 @@ void prof_after(int k, hipStream_t s) {
 }
 
 static CacheView view(const tv_cache &c) {
-  return CacheView{c.ring, c.c4, c.c4_idx, c.c128, c.c4_base, c.c128_base, c.c4_cap, c.c128_cap, c.len};
+  return CacheView{c.ring, c.c4, c.c4_idx, c.c128, c.c4_base, c.c128_base, c.c4_cap, c.c128_cap, c.len,
+                   c.page_table};
 }
 
 #define TV_LAUNCH(name, call)            \
@@ -227,7 +237,7 @@ static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const u
                               void *workspace, size_t workspace_bytes, hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
-  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
+  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
       !out || !row_status)
     return TV_ERR_INVALID_ARG;
   if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, row_status) ||
@@ -299,7 +309,7 @@ tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const u
                              hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
-  if (!cache_complete(cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
+  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
     return TV_ERR_INVALID_ARG;
   if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status) ||
       (primary_last && !a16(primary_last)))
@@ -345,7 +355,7 @@ tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const ui
                                   int32_t *row_status, const int32_t *primary_last, hipStream_t stream) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
-  if (!cache_complete(cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
+  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
       !accept_nodes || !accept_len || !row_status)
     return TV_ERR_INVALID_ARG;
   if (!cache_a16(cache) ||

@@ -7,7 +7,9 @@
 // so they leave no trace in the persistent state.
 //
 // One workgroup per row.  All checks run before the first write, so a failing
-// row is left exactly as it was.  The row's loads go out together; the copies
+// row is left exactly as it was.  Destinations follow the cache layout: the
+// ring and per-row pools, or with a paged pool the raw, CSA and HCA layers
+// through the row's page table (a page it does not allocate fails the row).  The row's loads go out together; the copies
 // (ring rows, CSA and HCA entries) form one list of 16-byte chunks whose
 // loads a thread issues before its stores.
 //
@@ -20,8 +22,7 @@
 // chain, or an accepted path that is the cached chain, needs no CSA refresh.
 // HCA entries are always written here, once the path is known, all of a
 // round's in one pass.
-#include "tv_common.h"
-#include "tv_internal.h"
+#include "pool_addr.h"
 
 namespace tv {
 
@@ -38,6 +39,7 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
   __shared__ int32_t path[64];
   __shared__ int32_t ent[2][64];  // closing path depths: CSA entries to copy, HCA entries
   __shared__ int nent[2];
+  __shared__ int64_t raw_at[64], slot_at[2][64];  // by path depth: raw-row index, CSA / HCA pool slot
   const int b = blockIdx.x, tid = threadIdx.x;
   const int64_t rb = (int64_t)b * d.D;
   // every independent load first, one wait for all of them
@@ -46,8 +48,9 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
   const int32_t last = accepted_last[b];
   const int32_t P = primary_last ? primary_last[b] : -1;
   const int32_t dt = tid < d.D ? depth[rb + tid] : 0;
-  const int32_t cap4 = c.c4_cap[b], cap128 = c.c128_cap[b];
-  const int64_t base4 = c.c4_base[b], base128 = c.c128_base[b];
+  const bool flat = d.page_size == 0;
+  const int32_t cap4 = flat ? c.c4_cap[b] : 0, cap128 = flat ? c.c128_cap[b] : 0;
+  const int64_t base4 = flat ? c.c4_base[b] : 0, base128 = flat ? c.c128_base[b] : 0;
   if (status != TV_ROW_OK) return;
   if (!len_ok(L, d.max_len)) {
     if (tid == 0) row_status[b] = TV_ROW_BAD_LEN;
@@ -62,11 +65,29 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
   const int a = depth[rb + last] + 1;
   if (tid < d.D && ((m >> tid) & 1ull)) path[dt] = tid;
   if (tid < 2) nent[tid] = 0;
+  // Destinations of the path's raw rows and of the entries it closes (flat:
+  // ring slot, base + index below the capacity; paged: through the page
+  // table), all resolved before any write: a missing one fails the row.
   bool bad = false;
   if (tid < a) {
     const int64_t p = (int64_t)L + tid;  // path node at depth tid stands at L + tid
-    if ((p + 1) % d.ratio_csa == 0 && (p + 1) / d.ratio_csa - 1 >= cap4) bad = true;
-    if ((p + 1) % d.ratio_hca == 0 && (p + 1) / d.ratio_hca - 1 >= cap128) bad = true;
+    const int64_t ri = raw_index(d, c.page_table, b, p);
+    raw_at[tid] = ri;
+    bad |= ri < 0;
+    if ((p + 1) % d.ratio_csa == 0) {
+      const int64_t s4 = (p + 1) / d.ratio_csa - 1;
+      const int64_t sl = flat ? (s4 < cap4 ? base4 + s4 : -1)
+                              : pool_slot(d, c.page_table, nullptr, nullptr, b, s4, d.ratio_csa);
+      slot_at[0][tid] = sl;
+      bad |= sl < 0;
+    }
+    if ((p + 1) % d.ratio_hca == 0) {
+      const int64_t s128 = (p + 1) / d.ratio_hca - 1;
+      const int64_t sl = flat ? (s128 < cap128 ? base128 + s128 : -1)
+                              : pool_slot(d, c.page_table, nullptr, nullptr, b, s128, d.ratio_hca);
+      slot_at[1][tid] = sl;
+      bad |= sl < 0;
+    }
   }
   if (__syncthreads_or(bad)) {
     if (tid == 0) row_status[b] = TV_ROW_CAPACITY;
@@ -108,11 +129,11 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
       if (e < n_ring) {
         const int t = e / cpr, cc = (e - t * cpr) * 8;
         v[u] = *reinterpret_cast<const uint4 *>(tree_u + (rb + path[t]) * d_u + cc);
-        dst[u] = c.ring + ((int64_t)b * d.ring_cap + ((L + t) & (d.ring_cap - 1))) * d_u + cc;
+        dst[u] = c.ring + raw_at[t] * d_u + cc;
       } else if (e < n_ring + n4) {
         const int x = e - n_ring, k = x / c4c, ch = (x - k * c4c) * 8;
         const int t = ent[0][k];
-        const int64_t slot = base4 + ((int64_t)L + t + 1) / d.ratio_csa - 1;
+        const int64_t slot = slot_at[0][t];
         v[u] = *reinterpret_cast<const uint4 *>(scr_c4 + (rb + path[t]) * d_u + ch);
         dst[u] = ch < d.d_row ? c.c4 + slot * d.d_row + ch : c.c4_idx + slot * d.d_idx + (ch - d.d_row);
         if (ch >= d.d_row && d.idx_fmt == TV_IDX_E4M3) {  // eight E4M3 codes: 8 bytes at byte offset slot*d_idx + ...
@@ -122,7 +143,7 @@ __global__ void __launch_bounds__(256) commit_kernel(tv_dims d, tv_cache c, cons
       } else if (e < total) {
         const int x = e - n_ring - n4, k = x / c128c, ch = (x - k * c128c) * 8;
         const int t = ent[1][k];
-        const int64_t slot = base128 + ((int64_t)L + t + 1) / d.ratio_hca - 1;
+        const int64_t slot = slot_at[1][t];
         v[u] = *reinterpret_cast<const uint4 *>(scr_c128 + (rb + path[t]) * d.d_row + ch);
         dst[u] = c.c128 + slot * d.d_row + ch;
       }

@@ -17,6 +17,10 @@
 // chunk) stream them with 16-byte loads, all of a thread's loads in flight
 // together.
 //
+// Committed rows come from the ring or, with a paged pool, from the raw
+// layer through the row's page table; a block whose committed rows lie in a
+// page the table does not allocate fails the row (TV_ROW_CAPACITY).
+//
 // With FP8 indexer keys the indexer channels of a CSA entry are rounded to
 // E4M3 (held in scratch as the same values in bfloat16, written to a pool
 // slot as E4M3 codes).
@@ -26,8 +30,7 @@
 // straight into their persistent pool slots.  Those slots lie past the
 // committed entries, so nothing reads them before the commit makes them
 // committed, and the commit then skips their copies.
-#include "tv_common.h"
-#include "tv_internal.h"
+#include "pool_addr.h"
 
 namespace tv {
 
@@ -70,8 +73,9 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   const int32_t dj = tid < d.D ? depth[(int64_t)b * d.D + tid] : 0;
   const uint64_t aj = (primary_last && tid < d.D) ? anc[(int64_t)b * d.D + tid] : 0ull;
   const int32_t P = primary_last ? primary_last[b] : -1;
-  const int32_t cap4 = primary_last ? c.c4_cap[b] : 0;
-  const int64_t base4 = primary_last ? c.c4_base[b] : 0;
+  const bool flat = d.page_size == 0;
+  const int32_t cap4 = (primary_last && flat) ? c.c4_cap[b] : 0;
+  const int64_t base4 = (primary_last && flat) ? c.c4_base[b] : 0;
   asm volatile("" ::"s"(cap4), "s"(base4));  // issued with the other loads
   const float g0 = tid < d_u ? bf2f(gate_w[tid]) : 0.f;
   const float g1 = tid < d_u ? bf2f(gate_w[d_u + tid]) : 0.f;
@@ -101,11 +105,17 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   }
   __syncthreads();
   const int64_t q0 = p - R + 1;
+  bool lost = false;  // a committed row of the block whose page is not allocated
   for (int t = tid; t < R; t += kNT) {
     const int64_t qq = q0 + t;
-    tok[t] = qq < L ? ring_row(c.ring, b, d.ring_cap, d_u, qq) : tree_u + ((int64_t)b * d.D + path[qq - L]) * d_u;
+    const int64_t ri = qq < L ? raw_index(d, c.page_table, b, qq) : 0;
+    lost |= ri < 0;
+    tok[t] = qq < L ? c.ring + (ri < 0 ? 0 : ri) * d_u : tree_u + ((int64_t)b * d.D + path[qq - L]) * d_u;
   }
-  __syncthreads();
+  if (__syncthreads_or(lost)) {
+    if (tid == 0) row_status[b] = TV_ROW_CAPACITY;
+    return;
+  }
 
   // Gate logits of every token for every ratio that pools it: 8 lanes per
   // token, 128 tokens per pass, all loads of a lane issued before their use.
@@ -212,8 +222,11 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   __syncthreads();
   // a CSA entry closed on the designated chain also goes to its pool slot, capacity permitting
   const int64_t slot4 = (p + 1) / d.ratio_csa - 1;
-  const bool through = cl[0] && ((chain_sh >> i) & 1ull) && slot4 < cap4;
-  const int64_t pslot = base4 + slot4;
+  int64_t pslot = -1;
+  if (cl[0] && ((chain_sh >> i) & 1ull))
+    pslot = flat ? (slot4 < cap4 ? base4 + slot4 : -1)
+                 : pool_slot(d, c.page_table, nullptr, nullptr, b, slot4, d.ratio_csa);
+  const bool through = pslot >= 0;
 #pragma unroll
   for (int ri = 0; ri < 2; ++ri) {
     if (!cl[ri]) continue;

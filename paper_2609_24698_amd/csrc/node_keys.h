@@ -12,7 +12,7 @@
 // (branch-aware causal visibility, Sec. 3.1).
 #pragma once
 
-#include "tv_common.h"
+#include "pool_addr.h"
 
 namespace tv {
 
@@ -79,27 +79,43 @@ __device__ inline NodeKeys node_keys(const tv_dims &d, int32_t L, int b, int i, 
   return k;
 }
 
+// Slot of committed entry s (s below the row's committed count) of the pool
+// of `ratio`: base + s flat, through the page table paged.  A page the table
+// does not allocate breaks the pool's contract; slot 0 keeps every read
+// inside the pool.
+__device__ __forceinline__ int64_t committed_slot(const tv_dims &d, const int32_t *page_table, int64_t base, int b,
+                                                  int64_t s, int ratio) {
+  if (d.page_size == 0) return base + s;
+  const int64_t v = pool_slot(d, page_table, nullptr, nullptr, b, s, ratio);
+  return v < 0 ? 0 : v;
+}
+
 // Pointer to the latent row (first d_row channels) of key t of the node.
+// c4_base and c128_base are the row's pool bases (flat layout only).
 __device__ inline const uint16_t *key_row(const tv_dims &d, const NodeKeys &k, int b, int t,
                                           const int32_t *sel_node, const int32_t *path, const int32_t *hca_node,
                                           const uint16_t *ring, const uint16_t *c4, const int64_t c4_base,
                                           const uint16_t *c128, const int64_t c128_base, const uint16_t *scr_c4,
-                                          const uint16_t *scr_c128, const uint16_t *tree_u) {
+                                          const uint16_t *scr_c128, const uint16_t *tree_u,
+                                          const int32_t *page_table) {
   const int d_u = d.d_row + d.d_idx;
   if (t < k.nsel) {
     int s = sel_node[t];
     if (s < 0) s = 0;  // defensive: a selection list is never shorter than nsel
-    if (s < k.n4) return c4 + (c4_base + s) * d.d_row;
+    if (s < k.n4) return c4 + committed_slot(d, page_table, c4_base, b, s, d.ratio_csa) * d.d_row;
     int64_t dd = (int64_t)(s + 1) * d.ratio_csa - 1 - k.L;
     if (dd < 0 || dd > k.p - k.L) dd = 0;  // defensive: stay on the node's own path
     return scr_c4 + ((int64_t)b * d.D + path[dd]) * d_u;
   }
   t -= k.nsel;
-  if (t < k.n128) return c128 + (c128_base + t) * d.d_row;
+  if (t < k.n128) return c128 + committed_slot(d, page_table, c128_base, b, t, d.ratio_hca) * d.d_row;
   t -= k.n128;
   if (t < k.s128) return scr_c128 + ((int64_t)b * d.D + hca_node[t]) * d.d_row;
   t -= k.s128;
-  if (t < k.nwin_c) return ring_row(ring, b, d.ring_cap, d_u, k.win_lo + t);
+  if (t < k.nwin_c) {
+    const int64_t ri = raw_index(d, page_table, b, k.win_lo + t);  // < 0 only if the page table breaks its contract
+    return ri < 0 ? tree_u + (int64_t)b * d.D * d_u : ring + ri * d_u;
+  }
   t -= k.nwin_c;
   const int64_t q = (k.win_lo > k.L ? k.win_lo : k.L) + t;
   return tree_u + ((int64_t)b * d.D + path[q - k.L]) * d_u;

@@ -12,8 +12,7 @@
 // list of all valid rows, so ragged lengths cost no idle workgroups.
 #include <algorithm>
 
-#include "tv_common.h"
-#include "tv_internal.h"
+#include "pool_addr.h"
 
 namespace tv {
 
@@ -111,7 +110,9 @@ __global__ void __launch_bounds__(256) score_kernel(tv_dims d, CacheView c, cons
     bf16x8 kb[4];
     {
       const bool live = e < n4;
-      const int64_t entry = c.c4_base[b] + (live ? e : 0);
+      const int64_t entry = d.page_size == 0 ? c.c4_base[b] + (live ? e : 0)
+                                             : std::max<int64_t>(0, pool_slot(d, c.page_table, nullptr, nullptr, b,
+                                                                              live ? e : 0, d.ratio_csa));
       uint4 raw[4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
@@ -195,7 +196,8 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
   const int M = d.D * 8;
   const int32_t status = row_status[b];
   const int32_t L = c.len[b];
-  const int64_t c4b = c.c4_base[b];
+  const bool flat = d.page_size == 0;
+  const int64_t c4b = flat ? c.c4_base[b] : 0;
   const float wv_ = tid < M ? bf2f(w_idx[(int64_t)b * M + tid]) : 0.f;
   if (status != TV_ROW_OK || !len_ok(L, d.max_len)) return;
   const int n4 = L / d.ratio_csa;
@@ -219,9 +221,17 @@ __global__ void __launch_bounds__(256) score_kernel_h8(tv_dims d, CacheView c, c
   // Every load is issued (entries past the row re-read its last one, which
   // exists: n4 > 0 here) and dead lanes are zeroed afterwards, so no branch
   // separates the loads and all of them are in flight together.
+  // With a paged pool each entry's slot comes from the row's page table
+  // first (a slot of a page the table lacks is clamped to slot 0).
+  int64_t ent[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int e = std::min(e0 + 8 * u + (lane >> 3), n4 - 1);
+    ent[u] = flat ? c4b + e : std::max<int64_t>(0, pool_slot(d, c.page_table, nullptr, nullptr, b, e, d.ratio_csa));
+  }
   uint4 kr[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) kr[u] = key_load<FP8>(c.c4_idx, c4b + std::min(e0 + 8 * u + (lane >> 3), n4 - 1), lane & 7);
+  for (int u = 0; u < 8; ++u) kr[u] = key_load<FP8>(c.c4_idx, ent[u], lane & 7);
 #pragma unroll
   for (int u = 0; u < 8; ++u)
     if (e0 + 8 * u + (lane >> 3) >= n4) kr[u] = make_uint4(0, 0, 0, 0);

@@ -228,8 +228,9 @@ __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n,
 // path entries from the scratch slot of the path node that closed them.
 __device__ __forceinline__ const uint16_t *csa_row(const tv_dims &d, const NodeKeys &nk, int b, int s,
                                                    const int32_t *path, const uint16_t *c4, int64_t c4b,
+                                                   const int32_t *page_table,
                                                    const uint16_t *scr_c4) {
-  if (s < nk.n4) return c4 + (c4b + s) * d.d_row;
+  if (s < nk.n4) return c4 + committed_slot(d, page_table, c4b, b, s, d.ratio_csa) * d.d_row;
   int64_t dd = (int64_t)(s + 1) * d.ratio_csa - 1 - nk.L;
   if (dd < 0 || dd > nk.p - nk.L) dd = 0;  // defensive: stay on the node's own path
   return scr_c4 + ((int64_t)b * d.D + path[dd]) * (d.d_row + d.d_idx);
@@ -273,7 +274,8 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
   const int32_t status = row_status[b];
   const int32_t L = c.len[b];
   const uint64_t m = anc[node];
-  const int64_t c4b = c.c4_base[b], c128b = c.c128_base[b];
+  const bool flat = d.page_size == 0;
+  const int64_t c4b = flat ? c.c4_base[b] : 0, c128b = flat ? c.c128_base[b] : 0;
   const int dl = lane < d.D ? depth[(int64_t)b * d.D + lane] : 0;  // depth of the row's node `lane`
   const int hl = lane >> 3, cc = lane & 7;  // path-entry scoring: head h0 + hl, channels 8cc..8cc+7
   uint4 qv0 = make_uint4(0, 0, 0, 0);
@@ -382,7 +384,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
   if (seg == 0) {
     for (int t = nk.nsel + tid; t < nk.n_keys; t += kTkNT)
       tab[t] = key_row(d, nk, b, t, nullptr, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128,
-                       tree_u);
+                       tree_u, c.page_table);
     if (tid == 0) {
       nkeys_tab[node] = nk.n_keys;
       nkeys_rank[rnode] = nk.n_keys;
@@ -407,7 +409,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
     for (int t = tid; t < k; t += kTkNT) {
       const int s = t < taken ? (all ? t : list[t]) : -1;  // one segment: element index = logical index
       out[t] = s;
-      if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, scr_c4);
+      if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, c.page_table, scr_c4);
     }
   } else {
     // survivors of this segment, in index order, then padding, for the merge
@@ -466,7 +468,7 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   const int total = real_cnt;
   const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
   const uint16_t **tab = keytab + ((int64_t)row_rank[b] * d.D + i) * keytab_stride;  // kept by (rank, node)
-  const int64_t c4b = c.c4_base[b];
+  const int64_t c4b = d.page_size == 0 ? c.c4_base[b] : 0;
   int32_t *out = sel + node * k;
   const bool all = total <= k;  // every real survivor (key above 0) is taken
   uint32_t prefix = 0u, pmask = 0xFFFFFFFFu;
@@ -478,7 +480,7 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   for (int t = tid; t < k; t += kTkNT) {
     const int s = t < taken ? surv_idx[sv + list[t]] : -1;
     out[t] = s;
-    if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, scr_c4);
+    if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, c.page_table, scr_c4);
   }
 }
 

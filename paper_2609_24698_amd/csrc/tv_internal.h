@@ -15,6 +15,7 @@ struct CacheView {
   const int64_t *c4_base, *c128_base;
   const int32_t *c4_cap, *c128_cap;
   const int32_t *len;
+  const int32_t *page_table;  // paged pool only (dims page_size > 0)
 };
 
 // Keys one attention workgroup takes per split (its LDS pointer table).

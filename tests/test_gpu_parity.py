@@ -130,6 +130,12 @@ SMALL_CASES = [
     dict(name="C0", B=3, D=8, tree="random", lens=[381, 3967, 1023], seed=44, topk=16, idx_fmt=1),
     dict(name="C1", B=2, D=8, lens=[1000, 3001], seed=45, topk=64, idx_fmt=1),
     dict(name="C1", B=2, D=12, tree="random", lens=[2043, 5119], seed=46, topk=128, H_idx=4, idx_fmt=1),
+    # the paged three-layer pool (raw rows, CSA and HCA entries through one page table per row)
+    dict(name="C0", lens=2047, page_size=128),
+    dict(name="C0", B=3, D=8, tree="random", lens=[381, 3967, 1023], seed=49, topk=16, page_size=256),
+    dict(name="C1", B=2, D=8, lens=[1000, 3007], seed=50, topk=64, page_size=128),
+    dict(name="C1", B=2, D=12, tree="random", lens=[2043, 5119], seed=51, topk=128, H_idx=4, idx_fmt=1,
+         page_size=128),
 ]
 
 

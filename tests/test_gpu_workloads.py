@@ -186,12 +186,13 @@ def test_indexer_variants(over):
     _check_stages(w, ref, r, rerun=_rerun(w, ref))
 
 
-@pytest.mark.parametrize("idx_fmt", [0, 1], ids=["bf16-keys", "fp8-keys"])
-def test_round_on_own_scratch(idx_fmt):
+@pytest.mark.parametrize("idx_fmt,page_size", [(0, 0), (1, 0), (1, 128)], ids=["bf16-keys", "fp8-keys",
+                                                                                "fp8-keys-paged"])
+def test_round_on_own_scratch(idx_fmt, page_size):
     """The whole round on the GPU's own intermediates: verify reads the GPU's
     scratch entries (which may differ from the oracle's in the last bit) and
     commit stores them."""
-    w = _small(B=4, lens=(1003, 2047, 1023, 3071), seed=74, idx_fmt=idx_fmt)
+    w = _small(B=4, lens=(1003, 2047, 1023, 3071), seed=74, idx_fmt=idx_fmt, page_size=page_size)
     ref = O.run_round(w)
     r = _device(w)
     r.round()
@@ -237,6 +238,33 @@ def test_c3_fp8_keys_full_size():
     ref = O.run_round(w, nodes)
     stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
     _say(f"  {stats}")
+
+
+def test_c3_paged_full_size():
+    """The ragged B=64 workload in a paged pool of 128-token pages, in the
+    benchmark's length bound: sampled rows, every row's commit."""
+    w = bench.bench_workload("C3", 20, 5, page_size=128)
+    assert w.page_table is not None
+    order = np.argsort(w.lens)
+    rows = sorted(set(int(b) for b in [order[-1], order[0], 0, 1, 2, 3, 17]))
+    nodes = [(b, i) for b in rows for i in range(w.D)]
+    _say(f"[workload] C3 paged rows={rows} lens={[int(w.lens[b]) for b in rows]}")
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
+
+
+def test_paged_row_errors():
+    """Paged pool: a row whose accepted path runs into a page its table does
+    not allocate fails with CAPACITY and keeps its state; a row with a bad
+    parent array fails on its own; the others commit."""
+    w = synth.make_workload("C1", B=3, D=5, lens=[127, 300, 1023], seed=52, topk=64, page_size=128)
+    w.accepted_last[:] = 3  # depth 2: positions L .. L+2
+    w.page_table[0, 1] = -1  # row 0: positions 128, 129 have no page
+    w.parents[1, 2] = 4
+    ref = O.run_round(w)
+    assert list(ref["commit"]["status"]) == [O.ROW_CAPACITY, O.ROW_BAD_PARENT, O.ROW_OK]
+    _check_stages(w, ref, _device(w), rerun=_rerun(w, ref))
 
 
 def test_c3_alt_shape_full_size():
