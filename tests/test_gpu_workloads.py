@@ -137,6 +137,28 @@ def test_softmax_restart(config):
     _say(f"  restart case: {stats}")
 
 
+def test_mla_stream_of_many_units():
+    """72 rows of the shared-latent shape (576 node units, more than two per
+    compute unit), lengths from a few hundred to a few thousand, and in every
+    third row a committed window key whose logits exceed the first tile's
+    maxima by far (those units restart from the larger reference)."""
+    rng = np.random.default_rng(78)
+    lens = rng.integers(300, 3000, size=72).tolist()
+    w = synth.make_workload("C1", B=72, D=8, lens=lens, seed=78, topk=128, tree="random")
+    cap, d_k, d_v = w.dims["ring_cap"], w.dims["d_k"], w.dims["d_v"]
+    for b in range(0, w.B, 3):
+        L = int(w.lens[b])
+        row = O.bf16_to_f64(w.ring[b, (L - 1) % cap])
+        row[d_v:d_k] *= 60.0  # rope channels only: keys, not values
+        w.ring[b, (L - 1) % cap] = O.f64_to_bf16(row)
+    rows = [0, 1, 3, 35, 69, 70, int(np.argmax(w.lens)), int(np.argmin(w.lens))]
+    nodes = [(b, i) for b in sorted(set(rows)) for i in range(w.D)]
+    _say(f"[workload] C1 shape B=72 stream rows={sorted(set(rows))}")
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  {stats}")
+
+
 def _small(B=5, D=8, lens=(1003, 2047, 999, 1023, 1500), seed=71, **over):
     return synth.make_workload("C1", B=B, D=D, lens=list(lens), seed=seed, topk=64, **over)
 
