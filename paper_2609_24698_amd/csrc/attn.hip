@@ -448,71 +448,94 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
 }
 
 // Merge the partials of nodes whose keys spanned several splits.  One
-// workgroup per (node, group of heads); a thread owns four value channels of
-// one head and streams that head's partials of every split with 16-byte
-// loads, weighting split s by exp2(m_s - m) / l (m the largest running
-// maximum, l the merged sum), summed in split order.
+// wavefront per (node, head, 64 CPL value channels), CPL = 4 for 512 value
+// channels (two wavefronts a head) and 2 for 128.  Lane s first holds split
+// s's running maximum and sum (64 splits at a time), so the merged maximum m
+// and sum l are wavefront reductions; split s then weighs exp2(m_s - m) / l
+// and the lane's CPL channels of every split's partial are summed in split
+// order, sixteen splits' loads in flight at a time.
 template <int DV>
 __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *__restrict__ row_status,
                                                       const int32_t *__restrict__ nkeys_tab, int chunk, int splits,
                                                       const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml, uint16_t *__restrict__ out,
                                                       float *__restrict__ lse) {
-  constexpr int kTPH = DV / 4;      // threads per head
-  constexpr int kHPW = 256 / kTPH;  // heads per workgroup
-  const int hgroups = (d.H + kHPW - 1) / kHPW;
-  const int nodeg = blockIdx.x / hgroups;
-  const int hg = blockIdx.x - nodeg * hgroups;
-  const int b = nodeg / d.D;
-  const int tid = threadIdx.x;
-  const int h = hg * kHPW + tid / kTPH, c4 = tid % kTPH;
-  const int32_t status = row_status[b];
-  const int n_keys = nkeys_tab[nodeg];
-  if (status != TV_ROW_OK || n_keys <= chunk || h >= d.H) return;
+  constexpr int kCPL = DV == 512 ? 4 : 2;  // value channels per lane
+  constexpr int kWPH = DV / (64 * kCPL);   // wavefronts per head
+  constexpr int kBatch = 16;               // splits whose partials are loaded together
+  const int lane = threadIdx.x & 63;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (node, head, part)
+  const int part = (int)(wid % kWPH);
+  const int64_t nh = wid / kWPH;
+  const int h = (int)(nh % d.H);
+  const int64_t node = nh / d.H;
+  if (node >= (int64_t)d.B * d.D) return;
+  const int b = (int)(node / d.D);
+  if (row_status[b] != TV_ROW_OK) return;
+  const int n_keys = nkeys_tab[node];
+  if (n_keys <= chunk) return;  // written by its only split
   const int used = (n_keys + chunk - 1) / chunk;
-  const int64_t node = nodeg;
   const float2 *ml = reinterpret_cast<const float2 *>(part_ml) + node * splits * d.H + h;  // split s at s * H
   float mx = -INFINITY;
-  for (int s = 0; s < used; ++s) mx = fmaxf(mx, ml[(int64_t)s * d.H].x);
+  for (int s0 = 0; s0 < used; s0 += 64)
+    if (s0 + lane < used) mx = fmaxf(mx, ml[(int64_t)(s0 + lane) * d.H].x);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   float l = 0.f;
-  for (int s = 0; s < used; ++s) {
-    const float2 v = ml[(int64_t)s * d.H];
-    l += exp2f(v.x - mx) * v.y;
-  }
-  const float4 *po = reinterpret_cast<const float4 *>(part_o) + (node * splits * d.H + h) * kTPH + c4;
-  const int64_t pstride = (int64_t)d.H * kTPH;  // next split, same head and channels
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  int s = 0;
-  for (; s + 4 <= used; s += 4) {  // four splits' loads in flight together
-    float4 o[4];
-    float w[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      o[k] = po[(s + k) * pstride];
-      w[k] = ml[(int64_t)(s + k) * d.H].x;
+  for (int s0 = 0; s0 < used; s0 += 64) {
+    float t = 0.f;
+    if (s0 + lane < used) {
+      const float2 v = ml[(int64_t)(s0 + lane) * d.H];
+      t = exp2f(v.x - mx) * v.y;
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float wk = exp2f(w[k] - mx) / l;
-      acc.x += wk * o[k].x;
-      acc.y += wk * o[k].y;
-      acc.z += wk * o[k].z;
-      acc.w += wk * o[k].w;
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+    l += t;
+  }
+  const float inv_l = 1.0f / l;
+  const int c0 = (part * 64 + lane) * kCPL;  // first value channel of the lane
+  const float *po = part_o + (node * splits * d.H + h) * DV + c0;
+  const int64_t pstride = (int64_t)d.H * DV;  // next split, same head and channels
+  float acc[kCPL] = {};
+  for (int s0 = 0; s0 < used; s0 += 64) {
+    float w = 0.f;  // lane j: weight of split s0 + j
+    if (s0 + lane < used) w = exp2f(ml[(int64_t)(s0 + lane) * d.H].x - mx) * inv_l;
+    const int n = std::min(64, used - s0);
+    for (int k0 = 0; k0 < n; k0 += kBatch) {
+      float o[kBatch][kCPL];
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int s = s0 + std::min(k0 + k, n - 1);  // past the last split: re-read it, weight 0
+        if constexpr (kCPL == 4) {
+          const float4 v = *reinterpret_cast<const float4 *>(po + s * pstride);
+          o[k][0] = v.x;
+          o[k][1] = v.y;
+          o[k][2] = v.z;
+          o[k][3] = v.w;
+        } else {
+          const float2 v = *reinterpret_cast<const float2 *>(po + s * pstride);
+          o[k][0] = v.x;
+          o[k][1] = v.y;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const float wk = k0 + k < n ? __shfl(w, k0 + k, 64) : 0.f;
+#pragma unroll
+        for (int c = 0; c < kCPL; ++c) acc[c] += wk * o[k][c];
+      }
     }
   }
-  for (; s < used; ++s) {
-    const float4 o = po[s * pstride];
-    const float wk = exp2f(ml[(int64_t)s * d.H].x - mx) / l;
-    acc.x += wk * o.x;
-    acc.y += wk * o.y;
-    acc.z += wk * o.z;
-    acc.w += wk * o.w;
+  uint16_t *dst = out + (node * d.H + h) * DV + c0;
+  if constexpr (kCPL == 4) {
+    uint2 packed;
+    packed.x = uint32_t(f2bf(acc[0])) | (uint32_t(f2bf(acc[1])) << 16);
+    packed.y = uint32_t(f2bf(acc[2])) | (uint32_t(f2bf(acc[3])) << 16);
+    *reinterpret_cast<uint2 *>(dst) = packed;
+  } else {
+    *reinterpret_cast<uint32_t *>(dst) = uint32_t(f2bf(acc[0])) | (uint32_t(f2bf(acc[1])) << 16);
   }
-  uint2 packed;
-  packed.x = uint32_t(f2bf(acc.x)) | (uint32_t(f2bf(acc.y)) << 16);
-  packed.y = uint32_t(f2bf(acc.z)) | (uint32_t(f2bf(acc.w)) << 16);
-  *reinterpret_cast<uint2 *>(out + (node * d.H + h) * DV + 4 * c4) = packed;
-  if (c4 == 0 && lse) lse[node * d.H + h] = (mx + __log2f(l)) * kLn2;
+  if (part == 0 && lane == 0 && lse) lse[node * d.H + h] = (mx + __log2f(l)) * kLn2;
 }
 
 template <int NW, int HT, int DK, int DV, int VOFF, int DROW>
@@ -541,8 +564,8 @@ hipError_t launch_attn(const tv_dims &d, const uint16_t *q, const int32_t *row_s
 hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s) {
   if (plan.splits <= 1) return hipSuccess;
-  const int hpw = 256 / (d.d_v / 4);
-  dim3 grid(d.B * d.D * ((d.H + hpw - 1) / hpw));
+  const int64_t waves = (int64_t)d.B * d.D * d.H * (d.d_v == 512 ? 2 : 1);
+  dim3 grid((unsigned)((waves + 3) / 4));
   if (d.d_v == 512)
     combine_kernel<512><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
                                              lse);

@@ -113,6 +113,34 @@ def test_segmented_topk(topk, zero_w):
         assert np.array_equal(sel[0, 3], np.arange(topk)) and np.array_equal(sel[1, 5], np.arange(topk))
 
 
+def test_topk_crowded_threshold():
+    """Committed indexer keys drawn from three distinct vectors, so each
+    node's scores take three values and the top-k threshold falls inside a
+    class of hundreds of exactly equal scores, which are taken lowest logical
+    index first.  Row 1 is long enough for two top-k segments and the
+    merge."""
+    w = synth.make_workload("C1", B=2, D=8, lens=[9001, 40003], seed=79, topk=512)
+    base = [w.c4_idx[int(w.c4_base[0]) + t].copy() for t in range(3)]
+    for b in range(w.B):
+        n4 = int(w.lens[b]) // w.dims["ratio_csa"]
+        c0 = int(w.c4_base[b])
+        for s_ in range(n4):
+            w.c4_idx[c0 + s_] = base[s_ % 3]
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    ref = O.run_round(w, nodes)
+    r = _device(w)
+    stats = _check_stages(w, ref, r, nodes, rerun=_rerun(w, ref))
+    # Equal scores are equal in both precisions here (same query, same key),
+    # so the selection is exact: score descending, then lower index.
+    sel, k = r.host("sel"), w.dims["topk"]
+    for (b, i) in nodes:
+        sc = ref["detail"][(b, i)]["scores"]
+        want = sorted(sorted(sc, key=lambda e: (-sc[e], e))[:k])
+        got = sel[b, i][sel[b, i] >= 0].tolist()
+        assert got == want, f"row {b} node {i}: tie order differs"
+    _say(f"  crowded threshold: {stats}")
+
+
 @pytest.mark.parametrize("config", ["C1", "C0"])
 def test_softmax_restart(config):
     """A committed window key whose logit exceeds the first tile's maximum by
