@@ -453,8 +453,9 @@ attn_kernel(tv_dims d, const uint16_t *__restrict__ q, const int32_t *__restrict
 // s's running maximum and sum (64 splits at a time), so the merged maximum m
 // and sum l are wavefront reductions; split s then weighs exp2(m_s - m) / l
 // and the lane's CPL channels of every split's partial are summed in split
-// order, sixteen splits' loads in flight at a time.
-template <int DV>
+// order, kBatch splits' loads in flight at a time (4, 8 or 16: the plan's
+// split count rounded up, so that a few splits cost few registers).
+template <int DV, int kBatch>
 __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *__restrict__ row_status,
                                                       const int32_t *__restrict__ nkeys_tab, int chunk, int splits,
                                                       const float *__restrict__ part_o,
@@ -462,7 +463,6 @@ __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *
                                                       float *__restrict__ lse) {
   constexpr int kCPL = DV == 512 ? 4 : 2;  // value channels per lane
   constexpr int kWPH = DV / (64 * kCPL);   // wavefronts per head
-  constexpr int kBatch = 16;               // splits whose partials are loaded together
   const int lane = threadIdx.x & 63;
   const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (node, head, part)
   const int part = (int)(wid % kWPH);
@@ -471,53 +471,72 @@ __global__ void __launch_bounds__(256) combine_kernel(tv_dims d, const int32_t *
   const int64_t node = nh / d.H;
   if (node >= (int64_t)d.B * d.D) return;
   const int b = (int)(node / d.D);
-  if (row_status[b] != TV_ROW_OK) return;
-  const int n_keys = nkeys_tab[node];
-  if (n_keys <= chunk) return;  // written by its only split
-  const int used = (n_keys + chunk - 1) / chunk;
   const float2 *ml = reinterpret_cast<const float2 *>(part_ml) + node * splits * d.H + h;  // split s at s * H
-  float mx = -INFINITY;
-  for (int s0 = 0; s0 < used; s0 += 64)
-    if (s0 + lane < used) mx = fmaxf(mx, ml[(int64_t)(s0 + lane) * d.H].x);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  float l = 0.f;
-  for (int s0 = 0; s0 < used; s0 += 64) {
-    float t = 0.f;
-    if (s0 + lane < used) {
-      const float2 v = ml[(int64_t)(s0 + lane) * d.H];
-      t = exp2f(v.x - mx) * v.y;
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
-    l += t;
-  }
-  const float inv_l = 1.0f / l;
   const int c0 = (part * 64 + lane) * kCPL;  // first value channel of the lane
   const float *po = part_o + (node * splits * d.H + h) * DV + c0;
   const int64_t pstride = (int64_t)d.H * DV;  // next split, same head and channels
+  // One round trip for the row state, the first 64 splits' (maximum, sum)
+  // (lane s holds split s's) and the first kBatch splits' partials; splits
+  // the node does not use are dropped once its key count is known.
+  const int32_t status = row_status[b];
+  const int n_keys = nkeys_tab[node];
+  const float2 ml0 = lane < splits ? ml[(int64_t)lane * d.H] : make_float2(-INFINITY, 0.f);
+  float o[kBatch][kCPL];
+  auto load_batch = [&](int s_first, int n_valid) {
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      if (k >= n_valid) {  // the same in every lane
+#pragma unroll
+        for (int c = 0; c < kCPL; ++c) o[k][c] = 0.f;
+        continue;
+      }
+      const float *src = po + (int64_t)(s_first + k) * pstride;
+      if constexpr (kCPL == 4) {
+        const float4 v = *reinterpret_cast<const float4 *>(src);
+        o[k][0] = v.x;
+        o[k][1] = v.y;
+        o[k][2] = v.z;
+        o[k][3] = v.w;
+      } else {
+        const float2 v = *reinterpret_cast<const float2 *>(src);
+        o[k][0] = v.x;
+        o[k][1] = v.y;
+      }
+    }
+  };
+  load_batch(0, std::min(kBatch, splits));
+  if (status != TV_ROW_OK) return;
+  if (n_keys <= chunk) return;  // written by its only split
+  const int used = (n_keys + chunk - 1) / chunk;
+#pragma unroll
+  for (int k = 0; k < kBatch; ++k)  // the prefetched partials of splits past `used` hold anything
+    if (k >= used)
+#pragma unroll
+      for (int c = 0; c < kCPL; ++c) o[k][c] = 0.f;
+  auto ml_at = [&](int s0) {  // lane's split s0 + lane, past `used`: (-inf, 0)
+    if (s0 + lane >= used) return make_float2(-INFINITY, 0.f);
+    return s0 == 0 ? ml0 : ml[(int64_t)(s0 + lane) * d.H];
+  };
+  float mx = -INFINITY;
+  for (int s0 = 0; s0 < used; s0 += 64) mx = fmaxf(mx, ml_at(s0).x);
+#pragma unroll
+  for (int o_ = 32; o_ > 0; o_ >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o_, 64));
+  float l = 0.f;
+  for (int s0 = 0; s0 < used; s0 += 64) {
+    const float2 v = ml_at(s0);
+    float t = s0 + lane < used ? exp2f(v.x - mx) * v.y : 0.f;
+#pragma unroll
+    for (int o_ = 32; o_ > 0; o_ >>= 1) t += __shfl_xor(t, o_, 64);
+    l += t;
+  }
+  const float inv_l = 1.0f / l;
   float acc[kCPL] = {};
   for (int s0 = 0; s0 < used; s0 += 64) {
-    float w = 0.f;  // lane j: weight of split s0 + j
-    if (s0 + lane < used) w = exp2f(ml[(int64_t)(s0 + lane) * d.H].x - mx) * inv_l;
+    const float2 v = ml_at(s0);
+    const float w = s0 + lane < used ? exp2f(v.x - mx) * inv_l : 0.f;  // lane j: weight of split s0 + j
     const int n = std::min(64, used - s0);
     for (int k0 = 0; k0 < n; k0 += kBatch) {
-      float o[kBatch][kCPL];
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int s = s0 + std::min(k0 + k, n - 1);  // past the last split: re-read it, weight 0
-        if constexpr (kCPL == 4) {
-          const float4 v = *reinterpret_cast<const float4 *>(po + s * pstride);
-          o[k][0] = v.x;
-          o[k][1] = v.y;
-          o[k][2] = v.z;
-          o[k][3] = v.w;
-        } else {
-          const float2 v = *reinterpret_cast<const float2 *>(po + s * pstride);
-          o[k][0] = v.x;
-          o[k][1] = v.y;
-        }
-      }
+      if (s0 + k0 > 0) load_batch(s0 + k0, std::min(kBatch, n - k0));
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) {
         const float wk = k0 + k < n ? __shfl(w, k0 + k, 64) : 0.f;
@@ -566,12 +585,16 @@ hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int
   if (plan.splits <= 1) return hipSuccess;
   const int64_t waves = (int64_t)d.B * d.D * d.H * (d.d_v == 512 ? 2 : 1);
   dim3 grid((unsigned)((waves + 3) / 4));
-  if (d.d_v == 512)
-    combine_kernel<512><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
-                                             lse);
+  auto go = [&](auto kernel) {
+    kernel<<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out, lse);
+  };
+  const bool wide = d.d_v == 512;
+  if (plan.splits <= 4)
+    wide ? go(combine_kernel<512, 4>) : go(combine_kernel<128, 4>);
+  else if (plan.splits <= 8)
+    wide ? go(combine_kernel<512, 8>) : go(combine_kernel<128, 8>);
   else
-    combine_kernel<128><<<grid, 256, 0, s>>>(d, row_status, nkeys, plan.chunk, plan.splits, part_o, part_ml, out,
-                                             lse);
+    wide ? go(combine_kernel<512, 16>) : go(combine_kernel<128, 16>);
   return hipGetLastError();
 }
 

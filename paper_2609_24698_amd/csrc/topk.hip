@@ -77,6 +77,8 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
   prefix = 0;
   pmask = 0;
   remaining = k;
+  // 13, 13 and 6 bits: every pass has at least the 16 bins per thread the scan reads
+  static_assert(32 % kTkBits >= 4, "no pass narrower than four bits");
   for (int shift = 32; shift > 0;) {
     const int nb = shift < kTkBits ? shift : kTkBits;
     const int sft = shift - nb;
@@ -407,7 +409,8 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
     // the node's selection (ascending, -1 padded) and its CSA key pointers
     int32_t *out = sel + node * k;
     for (int t = tid; t < k; t += kTkNT) {
-      const int s = t < taken ? (all ? t : list[t]) : -1;  // one segment: element index = logical index
+      // one segment: element index = logical index (a list entry stays inside the segment whatever it holds)
+      const int s = t < taken ? (all ? t : std::min(std::max(list[t], 0), seg_n - 1)) : -1;
       out[t] = s;
       if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, c.page_table, scr_c4);
     }
@@ -415,7 +418,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
     // survivors of this segment, in index order, then padding, for the merge
     const int64_t sv = ((int64_t)node * max_seg + seg) * k;
     for (int t = tid; t < k; t += kTkNT) {
-      const int e = t < taken ? (all ? t : list[t]) : -1;
+      const int e = t < taken ? (all ? t : std::min(std::max(list[t], 0), seg_n - 1)) : -1;
       surv_idx[sv + t] = e < 0 ? -1 : (e < cn ? c0 + e : n4 + (e - cn));
       surv_key[sv + t] = e < 0 ? 0u : live_key(e < cn ? sc[e] : scr_score[e - cn]);
     }
@@ -438,37 +441,49 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
                                                            const int32_t *__restrict__ surv_cnt) {
   __shared__ SelShared sh;
   __shared__ int real_cnt;
-  __shared__ int32_t path[64], hca_node[64], cnt[2];
-  const int tid = threadIdx.x;
+  __shared__ int32_t path[64], hca_node[64];
+  const int tid = threadIdx.x, lane = tid & 63;
   const int64_t node = blockIdx.x;
   const int b = (int)(node / d.D);
   const int i = (int)(node - (int64_t)b * d.D);
-  if (row_status[b] != TV_ROW_OK) return;
+  const int k = d.topk;
+  // One round trip for everything whose address is known from (row, node,
+  // lane): the row's state, the node's path, and all of the node's survivor
+  // slots and counts (those of segments the row does not have are dropped
+  // once its length is known).
+  const int32_t status = row_status[b];
   const int32_t L = c.len[b];
-  if (!len_ok(L, d.max_len)) return;
+  const int32_t rank = row_rank[b];
+  const int64_t c4b = d.page_size == 0 ? c.c4_base[b] : 0;
+  const uint64_t m = anc[node];
+  const int dl = lane < d.D ? depth[(int64_t)b * d.D + lane] : 0;
+  const int64_t sv = (int64_t)node * max_seg * k;
+  const int cnt_s = tid < max_seg ? surv_cnt[node * max_seg + tid] : 0;  // max_seg <= 64: wave 0
+  const int all_slots = max_seg * k;
+  const int nr_all = (all_slots + kTkNT - 1) / kTkNT;
+  uint32_t key[kTopkMergeKPT];
+#pragma unroll
+  for (int j = 0; j < kTopkMergeKPT; ++j)
+    key[j] = j < nr_all ? surv_key[sv + std::min(tid + kTkNT * j, all_slots - 1)] : 0u;
+  if (status != TV_ROW_OK || !len_ok(L, d.max_len)) return;
   const int n4 = L / d.ratio_csa;
   const int nseg = topk_segments(n4);
   if (nseg <= 1) return;
-  const int k = d.topk;
-  if (tid == 0) {
-    int run = 0;
-    for (int s = 0; s < nseg; ++s) run += surv_cnt[node * max_seg + s];
-    real_cnt = run;
-  }
   const int slots = nseg * k;
-  const int64_t sv = (int64_t)node * max_seg * k;
-  uint32_t key[kTopkMergeKPT];
 #pragma unroll
-  for (int j = 0; j < kTopkMergeKPT; ++j) {
-    const int e = tid + kTkNT * j;
-    const uint32_t kk = surv_key[sv + std::min(e, slots - 1)];
-    key[j] = e < slots ? kk : 0u;
+  for (int j = 0; j < kTopkMergeKPT; ++j)
+    if (tid + kTkNT * j >= slots) key[j] = 0u;
+  if (tid < 64) {
+    int run = tid < nseg ? cnt_s : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) run += __shfl_xor(run, o, 64);
+    if (tid == 0) real_cnt = run;
   }
-  __syncthreads();
+  uint64_t csa_mask;
+  const NodeKeys nk = path_keys(d, L, i, m, dl, path, hca_node, csa_mask);
+  __syncthreads();  // the survivor total and the node's path are visible
   const int total = real_cnt;
-  const NodeKeys nk = node_keys(d, L, b, i, anc, depth, path, hca_node, cnt);
-  const uint16_t **tab = keytab + ((int64_t)row_rank[b] * d.D + i) * keytab_stride;  // kept by (rank, node)
-  const int64_t c4b = d.page_size == 0 ? c.c4_base[b] : 0;
+  const uint16_t **tab = keytab + ((int64_t)rank * d.D + i) * keytab_stride;  // kept by (rank, node)
   int32_t *out = sel + node * k;
   const bool all = total <= k;  // every real survivor (key above 0) is taken
   uint32_t prefix = 0u, pmask = 0xFFFFFFFFu;
@@ -478,7 +493,7 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
   const int taken = all ? total : k;
   for (int t = tid; t < k; t += kTkNT) {
-    const int s = t < taken ? surv_idx[sv + list[t]] : -1;
+    const int s = t < taken ? surv_idx[sv + std::min(std::max(list[t], 0), slots - 1)] : -1;
     out[t] = s;
     if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, c.page_table, scr_c4);
   }
