@@ -113,6 +113,20 @@ def test_segmented_topk(topk, zero_w):
         assert np.array_equal(sel[0, 3], np.arange(topk)) and np.array_equal(sel[1, 5], np.arange(topk))
 
 
+@pytest.mark.parametrize("D", [8, 6, 1])
+def test_hca_blocks(D):
+    """Every row closes an HCA block inside its tree (committed lengths one to
+    D short of a multiple of 128), at every depth of the tree across the rows,
+    for a full binary-ish tree (D=8), a ragged one (D=6) and the root alone
+    (D=1); the entries match the oracle."""
+    lens = [128 * (k + 8) - 1 - (k % D) for k in range(12)]
+    w = synth.make_workload("C1", B=len(lens), D=D, lens=lens, seed=80 + D, topk=64, tree="random")
+    nodes = [(b, i) for b in range(w.B) for i in range(w.D)]
+    ref = O.run_round(w, nodes)
+    stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
+    _say(f"  HCA blocks D={D}: {stats}")
+
+
 def test_topk_crowded_threshold():
     """Committed indexer keys drawn from three distinct vectors, so each
     node's scores take three values and the top-k threshold falls inside a
