@@ -1,8 +1,9 @@
 """Benchmark of one verify round per step on one MI355X.
 
 A step is the whole hot path over one batch: tree mask, per-branch
-compression, verify attention and accepted-path commit, for B rows of D-node
-draft trees.  Every step commits its accepted path, so the committed context
+compression and verify attention in one library call (the mask and the
+indexer scoring share a launch), then the accepted-path commit, for B rows of
+D-node draft trees.  Every step commits its accepted path, so the committed context
 grows by the accepted length (at most D tokens per row per step) like a
 decoding loop would.  Inputs are synthetic and already resident in HBM.
 
@@ -23,9 +24,9 @@ timed on a bounded sample of the same workload.  Under "next_rows" it adds the
 other workloads (each its own cold/warm step time and attention roofline,
 the B=32 tree against its chain twin on identical bytes, and the 8-head
 reading of the ragged workload), the greedy accepted-path selection over the
-same trees, the refresh schedule, and a round over 61 layers issued call by
-call against the same round replayed as one HIP graph; none of them is part
-of the step.
+same trees, the refresh schedule (each stage its own call, so the compression
+is timed alone), and a round over 61 layers issued call by call against the
+same round replayed as one HIP graph; none of them is part of the step.
 """
 from __future__ import annotations
 
@@ -210,7 +211,7 @@ def bench_workload(config: str, steps: int, warmup: int, seed=None, **over):
     for every step's commit (at most D tokens per row per step)."""
     import synth
 
-    grow = (5 * steps + warmup + 2) * synth.CONFIGS[config]["D"]  # five timed regions of K steps
+    grow = (6 * steps + warmup + 2) * synth.CONFIGS[config]["D"]  # six timed regions of K steps
     return synth.make_workload(config, seed=seed, max_len_margin=grow, extra_c4=grow // 4 + 8,
                                extra_c128=grow // 128 + 4, **over)
 
@@ -294,9 +295,7 @@ def measure(wl, K, W, torch, binding, flush):
     from paper_2609_24698_amd import DeviceRound
 
     r = DeviceRound(wl, "cuda:0", poison_outputs=False)
-    r.mask()
-    r.compress()
-    r.verify()
+    r.verify_round()
     torch.cuda.synchronize()
     st = r.host("row_status")
     assert np.all(st == 0), f"rows failed: {np.unique(st)}"
@@ -374,17 +373,23 @@ def time_selection(r, wl, K, binding, torch):
                          "avg_launch_ms": round(avg, 5)}}
 
 
-def time_refresh(r, wl, K, binding, torch, plain_kern):
+def time_refresh(r, wl, K, binding, torch):
     """The refresh schedule with every row's accepted path designated as its
-    cached chain (the case where the CSA refresh is skipped entirely): K more
-    whole steps with per-kernel HIP events, against the plain steps."""
+    cached chain (the case where the CSA refresh is skipped entirely): K whole
+    steps with per-kernel HIP events, plain then designated, each stage its
+    own call so the compression is timed alone."""
+    def kernels():
+        binding.tv_profile_enable(8 * K + 16)
+        for _ in range(K):
+            r.round_calls()
+        torch.cuda.synchronize()
+        kern = binding.tv_profile_read()
+        binding.tv_profile_disable()
+        return kern
+
+    plain_kern = kernels()
     r.set_primary(wl.accepted_last)
-    binding.tv_profile_enable(8 * K + 16)
-    for _ in range(K):
-        r.round()
-    torch.cuda.synchronize()
-    kern = binding.tv_profile_read()
-    binding.tv_profile_disable()
+    kern = kernels()
     r.set_primary(None)
     status = r.host("row_status")
     assert np.all(status == 0), f"rows left the workload: {np.unique(status)}"
@@ -527,7 +532,7 @@ def main():
             nxt["select_accepted_path"] = sel
             print(f"[bench] selection: {sel['ms_per_call']:.4f} ms per call, argmax "
                   f"{sel['roofline']['achieved']:.0f} GB/s", file=sys.stderr, flush=True)
-        nxt["refresh_schedule"] = time_refresh(r, wl, K, binding, torch, m["kern_warm"])
+        nxt["refresh_schedule"] = time_refresh(r, wl, K, binding, torch)
     del r, m
     torch.cuda.empty_cache()
     if not args.no_next and not args.no_workloads:

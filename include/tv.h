@@ -20,6 +20,9 @@
  *   tv_commit_accepted_path  accepted-path refresh of token window, CSA and HCA
  *                            state; rejected branches leave no trace (Sec. 3.2,
  *                            Sec. 4.2)
+ *   tv_verify_round          mask, compression and verification of one layer in
+ *                            one call, the indexer scoring in the mask's launch
+ *                            (Sec. 4.1, Sec. 4.3)
  *
  * Reading of the compressed-attention arithmetic (the paper cites DeepSeek-V4
  * for it): a ratio-r entry pools the r raw rows of a block with softmax
@@ -34,7 +37,8 @@
  * Conventions shared by every call
  *   - Every pointer is device memory owned by the caller.  The library never
  *     allocates device memory and keeps no state between calls besides device
- *     properties and the optional profiling records.
+ *     properties, the array of tv_verify_attention_noalloc and the optional
+ *     profiling records.
  *   - Every buffer must start on a 16-byte boundary (the kernels move rows
  *     with 16-byte accesses); a misaligned pointer is TV_ERR_INVALID_ARG.
  *   - The verify workspace must be 256-byte aligned.
@@ -286,7 +290,8 @@ tv_status tv_select_accepted_path(const tv_dims *dims, const int32_t *parents, c
  * verify preprocess once, then per layer the branch compression and verify
  * attention, then (optionally) the greedy path selection, then per layer the
  * commit.  tv_round_graph_create records that whole sequence, with every
- * argument check done once, into one HIP graph; tv_round_graph_launch replays
+ * argument check done once, into one HIP graph (each layer as tv_verify_round
+ * runs it); tv_round_graph_launch replays
  * it on any stream.  A graph is bound to its dims (B, D, max_len: the "D
  * bucket") and to the buffer addresses given at creation; the tree shape,
  * token contents and lengths are read from device memory at replay, so new
@@ -323,6 +328,23 @@ typedef struct {
   void *select_workspace;
   size_t select_workspace_bytes;
 } tv_round;
+
+/* Verify preprocess, branch compression and verify attention of one layer
+ * (Sec. 4.1: mask, then per-branch compression, then branch-aware causal
+ * attention) in one call, with the same results, bit for bit, as
+ * tv_build_tree_mask, tv_branch_compress and tv_verify_attention issued in
+ * that order on `stream` with the same arguments.  The indexer scoring reads
+ * only committed CSA keys and the indexer queries, neither the masks nor the
+ * compression's output, so where its fast path applies (H_idx = 8, D <= 8)
+ * it runs in the same kernel launch as the mask, one launch fewer per step
+ * (overlap of independent device work, Sec. 4.3).  Everything runs on `stream`, in order
+ * with earlier and later work on it.  The selection inputs of `round`
+ * (draft_tokens, target_logits, ...) and accepted_last, accept_nodes,
+ * accept_len are not used.  With round->parents NULL the mask is not built:
+ * anc and depth are inputs that already hold this round's tree (the later
+ * layers of a model that share it).  Every check of the three calls runs
+ * before anything is launched. */
+tv_status tv_verify_round(const tv_dims *dims, const tv_round *round, const tv_layer *layer, hipStream_t stream);
 
 typedef struct tv_round_graph tv_round_graph;
 

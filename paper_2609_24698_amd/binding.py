@@ -21,7 +21,7 @@ ROW_OK, ROW_BAD_PARENT, ROW_BAD_ACCEPT, ROW_CAPACITY, ROW_BAD_LEN = range(5)
 
 EXPORTED = (
     "tv_build_tree_mask", "tv_branch_compress", "tv_verify_workspace_bytes", "tv_verify_attention",
-    "tv_verify_attention_noalloc",
+    "tv_verify_attention_noalloc", "tv_verify_round",
     "tv_commit_accepted_path", "tv_select_workspace_bytes", "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_kernels",
     "tv_round_graph_launch", "tv_round_graph_destroy", "tv_status_string", "tv_profile_enable", "tv_profile_disable", "tv_profile_read",
 )
@@ -85,6 +85,7 @@ def lib() -> ctypes.CDLL:
         L.tv_select_workspace_bytes.argtypes = [dp, i32]
         L.tv_select_workspace_bytes.restype = sz
         L.tv_select_accepted_path.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.tv_verify_round.argtypes = [dp, ctypes.POINTER(TvRound), ctypes.POINTER(TvLayer), vp]
         L.tv_round_graph_create.argtypes = [dp, ctypes.POINTER(TvRound), ctypes.POINTER(TvLayer), i32,
                                             ctypes.POINTER(vp)]
         L.tv_round_graph_kernels.argtypes = [vp]
@@ -96,7 +97,7 @@ def lib() -> ctypes.CDLL:
         L.tv_profile_enable.argtypes = [i32]
         L.tv_profile_read.argtypes = [ctypes.POINTER(TvKernelTime), i32, ctypes.POINTER(i32)]
         for name in ("tv_build_tree_mask", "tv_branch_compress", "tv_verify_attention", "tv_verify_attention_noalloc",
-                     "tv_commit_accepted_path",
+                     "tv_verify_round", "tv_commit_accepted_path",
                      "tv_select_accepted_path", "tv_round_graph_create", "tv_round_graph_launch",
                      "tv_round_graph_destroy", "tv_profile_enable", "tv_profile_disable", "tv_profile_read"):
             getattr(L, name).restype = ctypes.c_int
@@ -130,6 +131,10 @@ def _ptr(t: Optional[torch.Tensor], dtype=None) -> Optional[int]:
     if dtype is not None and t.dtype != dtype:
         raise ValueError(f"expected {dtype}, got {t.dtype}")
     return t.data_ptr()
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
 
 
 def _stream(stream) -> Optional[int]:
@@ -241,6 +246,26 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(a).to(device)
 
 
+def layer_struct(cache: TvCache, t) -> TvLayer:
+    """The TvLayer of one layer's buffers (``t``: DeviceRound.t)."""
+    return TvLayer(cache, _ptr(t["tree_u"]), _ptr(t["gate_w"]), _ptr(t["q"]), _ptr(t["q_idx"]), _ptr(t["w_idx"]),
+                   _ptr(t["scr_c4"]), _ptr(t["scr_c128"]), _ptr(t["out"]), _ptr(t["lse"]), _ptr(t["sel"]),
+                   _ptr(t["workspace"]), _nbytes(t["workspace"]))
+
+
+def round_struct(t, parents, vocab: int = 0) -> TvRound:
+    """The TvRound of the shared tree buffers ``t`` (a DeviceRound.t), with
+    the selection buffers when ``t`` holds target logits."""
+    sel = "target_logits" in t
+    return TvRound(_ptr(parents), _ptr(t["anc"]), _ptr(t["depth"]), _ptr(t["row_status"]),
+                   _ptr(t["accepted_last"]), _ptr(t["accept_nodes"]), _ptr(t["accept_len"]),
+                   _ptr(t.get("primary_last"), torch.int32),
+                   _ptr(t["draft_tokens"]) if sel else None, _ptr(t["target_logits"]) if sel else None,
+                   vocab if sel else 0, _ptr(t["target_tokens"]) if sel else None,
+                   _ptr(t["next_token"]) if sel else None, _ptr(t["select_ws"]) if sel else None,
+                   _nbytes(t["select_ws"]) if sel else 0)
+
+
 class DeviceRound:
     """Device buffers of one verify round built from host arrays.
 
@@ -313,6 +338,16 @@ class DeviceRound:
                                     t["lse"] if with_lse else None, t["sel"] if with_sel else None,
                                     t["row_status"], stream)
 
+    def verify_round(self, stream=None, with_mask: bool = True):
+        """mask + compress + verify in one library call (tv_verify_round):
+        the indexer scoring runs beside the compression.  ``with_mask=False``
+        reuses the masks already in anc/depth."""
+        t = self.t
+        rnd = round_struct(t, t["parents"] if with_mask else None, getattr(self, "vocab", 0))
+        layer = layer_struct(self.cache, t)
+        _check(lib().tv_verify_round(ctypes.byref(self.dims), ctypes.byref(rnd), ctypes.byref(layer),
+                                     _stream(stream)), "tv_verify_round")
+
     def commit(self, stream=None):
         t = self.t
         tv_commit_accepted_path(self.dims, self.cache, t["tree_u"], t["anc"], t["depth"], t["scr_c4"],
@@ -342,6 +377,15 @@ class DeviceRound:
                                 t["next_token"] if with_next else None, t["row_status"], t["select_ws"], stream)
 
     def round(self, stream=None):
+        """One step: mask, compression and verification in one call, then
+        selection (when attached) and commit."""
+        self.verify_round(stream)
+        if "target_logits" in self.t:
+            self.select(stream)
+        self.commit(stream)
+
+    def round_calls(self, stream=None):
+        """round() issued one library call per stage, all on ``stream``."""
         self.mask(stream)
         self.compress(stream)
         self.verify(stream)
@@ -361,10 +405,6 @@ class DeviceRound:
 # ---------------------------------------------------------------------------
 # A round over several layers: shared tree buffers, per-layer state.
 # ---------------------------------------------------------------------------
-def _nbytes(t: torch.Tensor) -> int:
-    return t.numel() * t.element_size()
-
-
 class LayeredRound:
     """One verify round over several layers that share a draft tree.
 
@@ -384,9 +424,23 @@ class LayeredRound:
     def _shared(self):
         return self.layers[0].t
 
-    def eager(self, stream=None):
+    def eager(self, stream=None, fused: bool = True):
+        """The round call by call.  ``fused``: per layer one tv_verify_round
+        (the mask with layer 0), as the graph records it; otherwise mask,
+        compress and verify as separate calls on one stream."""
         t0 = self._shared()
-        L0 = self.layers[0]
+        if fused:
+            for k, r in enumerate(self.layers):
+                rnd = round_struct(t0, t0["parents"] if k == 0 else None)
+                layer = layer_struct(r.cache, r.t)
+                _check(lib().tv_verify_round(ctypes.byref(self.dims), ctypes.byref(rnd), ctypes.byref(layer),
+                                             _stream(stream)), "tv_verify_round")
+        else:
+            self._calls(stream)
+        self._finish(stream)
+
+    def _calls(self, stream):
+        t0 = self._shared()
         tv_build_tree_mask(self.dims, t0["parents"], t0["anc"], t0["depth"], t0["row_status"], stream)
         for r in self.layers:
             t = r.t
@@ -395,6 +449,10 @@ class LayeredRound:
             tv_verify_attention(self.dims, r.cache, t["tree_u"], t0["anc"], t0["depth"], t["scr_c4"], t["scr_c128"],
                                 t["q"], t["q_idx"], t["w_idx"], t["out"], t["lse"], t["sel"], t0["row_status"],
                                 t["workspace"], stream)
+
+    def _finish(self, stream):
+        t0 = self._shared()
+        L0 = self.layers[0]
         if "target_logits" in t0:
             tv_select_accepted_path(self.dims, t0["parents"], t0["anc"], t0["depth"], t0["draft_tokens"],
                                     t0["target_logits"], L0.vocab, t0["target_tokens"], t0["accepted_last"],
@@ -410,18 +468,8 @@ class LayeredRound:
         t0 = self._shared()
         layers = (TvLayer * len(self.layers))()
         for k, r in enumerate(self.layers):
-            t = r.t
-            layers[k] = TvLayer(r.cache, _ptr(t["tree_u"]), _ptr(t["gate_w"]), _ptr(t["q"]), _ptr(t["q_idx"]),
-                                _ptr(t["w_idx"]), _ptr(t["scr_c4"]), _ptr(t["scr_c128"]), _ptr(t["out"]),
-                                _ptr(t["lse"]), _ptr(t["sel"]), _ptr(t["workspace"]), _nbytes(t["workspace"]))
-        sel = "target_logits" in t0
-        rnd = TvRound(_ptr(t0["parents"]), _ptr(t0["anc"]), _ptr(t0["depth"]), _ptr(t0["row_status"]),
-                      _ptr(t0["accepted_last"]), _ptr(t0["accept_nodes"]), _ptr(t0["accept_len"]),
-                      _ptr(t0.get("primary_last"), torch.int32),
-                      _ptr(t0["draft_tokens"]) if sel else None, _ptr(t0["target_logits"]) if sel else None,
-                      self.layers[0].vocab if sel else 0, _ptr(t0["target_tokens"]) if sel else None,
-                      _ptr(t0["next_token"]) if sel else None, _ptr(t0["select_ws"]) if sel else None,
-                      _nbytes(t0["select_ws"]) if sel else 0)
+            layers[k] = layer_struct(r.cache, r.t)
+        rnd = round_struct(t0, t0["parents"], getattr(self.layers[0], "vocab", 0))
         self._keep = (layers, rnd)
         h = ctypes.c_void_p()
         _check(lib().tv_round_graph_create(ctypes.byref(self.dims), ctypes.byref(rnd), layers, len(self.layers),

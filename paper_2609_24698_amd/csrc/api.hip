@@ -191,13 +191,14 @@ static CacheView view(const tv_cache &c) {
                    c.page_table};
 }
 
-#define TV_LAUNCH(name, call)            \
-  do {                                   \
-    const int k_ = prof_before(name, stream); \
-    hipError_t e_ = (call);              \
-    prof_after(k_, stream);              \
+#define TV_LAUNCH_ON(name, call, strm)    \
+  do {                                    \
+    const int k_ = prof_before(name, strm); \
+    hipError_t e_ = (call);               \
+    prof_after(k_, strm);                 \
     if (e_ != hipSuccess) return TV_ERR_LAUNCH; \
   } while (0)
+#define TV_LAUNCH(name, call) TV_LAUNCH_ON(name, call, stream)
 
 }  // namespace tv
 
@@ -230,11 +231,35 @@ static tv_status noalloc_scratch(void **ptr) {
   return TV_OK;
 }
 
-static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+// Argument checks of the mask and compression calls (no launch).
+static tv_status mask_check(const tv_dims *dims, const int32_t *parents, const uint64_t *anc, const int32_t *depth,
+                            const int32_t *row_status) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!parents || !anc || !depth || !row_status) return TV_ERR_INVALID_ARG;
+  if (!all_a16(parents, anc, depth, row_status)) return TV_ERR_INVALID_ARG;
+  return check_device();
+}
+static tv_status compress_check(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                                const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w,
+                                const uint16_t *scr_c4, const uint16_t *scr_c128, const int32_t *row_status,
+                                const int32_t *primary_last) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status) ||
+      (primary_last && !a16(primary_last)))
+    return TV_ERR_INVALID_ARG;
+  return check_device();
+}
+
+// Argument checks of the verify call (no launch).
+static tv_status verify_check(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
                               const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
                               const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
                               const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel, int32_t *row_status,
-                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+                              void *workspace, size_t workspace_bytes) {
   tv_status st = check_dims(dims);
   if (st != TV_OK) return st;
   if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !q || !q_idx || !w_idx ||
@@ -246,15 +271,31 @@ static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const u
   const WsLayout w = ws_layout(*dims);
   if (!workspace || workspace_bytes < w.total) return TV_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) & 255) return TV_ERR_INVALID_ARG;
-  if ((st = check_device()) != TV_OK) return st;
-  const tv_dims &d = *dims;
+  return check_device();
+}
+
+// The verify call's first kernel, the indexer scoring: it reads the committed
+// state and the indexer queries only, not the compression's scratch.
+static tv_status verify_score(const tv_dims &d, const tv_cache *cache, const uint16_t *q_idx, const uint16_t *w_idx,
+                              int32_t *row_status, void *workspace, hipStream_t stream) {
+  const WsLayout w = ws_layout(d);
+  float *scores = reinterpret_cast<float *>(static_cast<char *>(workspace) + w.scores);
+  TV_LAUNCH("indexer_score", launch_score(d, view(*cache), q_idx, w_idx, row_status, scores, w.score_stride, stream));
+  return TV_OK;
+}
+
+// The rest of the verify call: selection (and merge), attention (and combine).
+static tv_status verify_rest(const tv_dims &d, const tv_cache *cache, const uint16_t *tree_u, const uint64_t *anc,
+                             const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
+                             const uint16_t *q_idx, const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel,
+                             int32_t *row_status, void *workspace, hipStream_t stream) {
+  const WsLayout w = ws_layout(d);
   char *ws = static_cast<char *>(workspace);
   float *scores = reinterpret_cast<float *>(ws + w.scores);
   int32_t *selp = sel ? sel : reinterpret_cast<int32_t *>(ws + w.sel);
   float *part_o = reinterpret_cast<float *>(ws + w.part_o);
   float *part_ml = reinterpret_cast<float *>(ws + w.part_ml);
   const CacheView cv = view(*cache);
-  TV_LAUNCH("indexer_score", launch_score(d, cv, q_idx, w_idx, row_status, scores, w.score_stride, stream));
   int32_t *row_order = reinterpret_cast<int32_t *>(ws + w.row_order);
   int32_t *row_rank = reinterpret_cast<int32_t *>(ws + w.row_rank);
   const uint16_t **keytab = reinterpret_cast<const uint16_t **>(ws + w.keytab);
@@ -276,6 +317,56 @@ static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const u
   return TV_OK;
 }
 
+static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                              const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                              const uint16_t *scr_c128, const uint16_t *q, const uint16_t *q_idx,
+                              const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel, int32_t *row_status,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  tv_status st = verify_check(dims, cache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, lse, sel,
+                              row_status, workspace, workspace_bytes);
+  if (st != TV_OK) return st;
+  if ((st = verify_score(*dims, cache, q_idx, w_idx, row_status, workspace, stream)) != TV_OK) return st;
+  return verify_rest(*dims, cache, tree_u, anc, depth, scr_c4, scr_c128, q, q_idx, w_idx, out, lse, sel, row_status,
+                     workspace, stream);
+}
+
+// One layer's verify preprocess (with_mask), compression and verification.
+// With the mask and the scoring's fast path, the mask and the indexer
+// scoring (which reads neither the masks nor the compression's output) are
+// one launch, then the compression, then the rest; otherwise the calls'
+// kernels in the calls' order.  Every kernel computes what it computes in the
+// separate calls, so the results are the same bits.  Arguments already
+// checked.
+static tv_status layer_step(const tv_dims *d, const tv_round &r, const tv_layer &L, bool with_mask,
+                            hipStream_t stream) {
+  const bool fused = with_mask && score_fast_path(*d);
+  if (fused) {
+    const WsLayout w = ws_layout(*d);
+    float *scores = reinterpret_cast<float *>(static_cast<char *>(L.workspace) + w.scores);
+    TV_LAUNCH("mask_score", launch_mask_score(*d, r.parents, r.anc, r.depth, r.row_status, view(L.cache), L.q_idx,
+                                              L.w_idx, scores, w.score_stride, stream));
+  } else if (with_mask) {
+    TV_LAUNCH("tree_mask", launch_mask(*d, r.parents, r.anc, r.depth, r.row_status, stream));
+  }
+  TV_LAUNCH("branch_compress", launch_compress(*d, view(L.cache), L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4,
+                                               L.scr_c128, r.row_status, r.primary_last, L.cache.c4, L.cache.c4_idx,
+                                               stream));
+  if (!fused) {
+    const tv_status st = verify_score(*d, &L.cache, L.q_idx, L.w_idx, r.row_status, L.workspace, stream);
+    if (st != TV_OK) return st;
+  }
+  return verify_rest(*d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx, L.out,
+                     L.lse, L.sel, r.row_status, L.workspace, stream);
+}
+
+static tv_status layer_check(const tv_dims *d, const tv_round &r, const tv_layer &L) {
+  tv_status st = compress_check(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status,
+                                r.primary_last);
+  if (st != TV_OK) return st;
+  return verify_check(d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx, L.out,
+                      L.lse, L.sel, r.row_status, L.workspace, L.workspace_bytes);
+}
+
 }  // namespace tv
 
 extern "C" {
@@ -294,11 +385,8 @@ const char *tv_status_string(int s) {
 
 tv_status tv_build_tree_mask(const tv_dims *dims, const int32_t *parents, uint64_t *anc, int32_t *depth,
                              int32_t *row_status, hipStream_t stream) {
-  tv_status st = check_dims(dims);
+  const tv_status st = mask_check(dims, parents, anc, depth, row_status);
   if (st != TV_OK) return st;
-  if (!parents || !anc || !depth || !row_status) return TV_ERR_INVALID_ARG;
-  if (!all_a16(parents, anc, depth, row_status)) return TV_ERR_INVALID_ARG;
-  if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("tree_mask", launch_mask(*dims, parents, anc, depth, row_status, stream));
   return TV_OK;
 }
@@ -307,17 +395,21 @@ tv_status tv_branch_compress(const tv_dims *dims, const tv_cache *cache, const u
                              const uint64_t *anc, const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4,
                              uint16_t *scr_c128, int32_t *row_status, const int32_t *primary_last,
                              hipStream_t stream) {
-  tv_status st = check_dims(dims);
+  tv_status st = compress_check(dims, cache, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status, primary_last);
   if (st != TV_OK) return st;
-  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !gate_w || !scr_c4 || !scr_c128 || !row_status)
-    return TV_ERR_INVALID_ARG;
-  if (!cache_a16(cache) || !all_a16(tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status) ||
-      (primary_last && !a16(primary_last)))
-    return TV_ERR_INVALID_ARG;
-  if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("branch_compress", launch_compress(*dims, view(*cache), tree_u, anc, depth, gate_w, scr_c4, scr_c128,
                                                row_status, primary_last, cache->c4, cache->c4_idx, stream));
   return TV_OK;
+}
+
+tv_status tv_verify_round(const tv_dims *dims, const tv_round *round, const tv_layer *layer, hipStream_t stream) {
+  if (!round || !layer) return TV_ERR_INVALID_ARG;
+  const bool with_mask = round->parents != nullptr;  // NULL: anc and depth already hold this round's mask
+  tv_status st = layer_check(dims, *round, *layer);
+  if (st != TV_OK) return st;
+  if (with_mask && (st = mask_check(dims, round->parents, round->anc, round->depth, round->row_status)) != TV_OK)
+    return st;
+  return layer_step(dims, *round, *layer, with_mask, stream);
 }
 
 size_t tv_verify_workspace_bytes(const tv_dims *dims) {
@@ -411,14 +503,9 @@ namespace tv {
 
 // The calls of one round, in order, on stream s (argument checks included).
 static tv_status record_round(const tv_dims *d, const tv_round &r, const tv_layer *layers, int n, hipStream_t s) {
-  tv_status st = tv_build_tree_mask(d, r.parents, r.anc, r.depth, r.row_status, s);
-  for (int l = 0; l < n && st == TV_OK; ++l) {
-    const tv_layer &L = layers[l];
-    st = tv_branch_compress(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status,
-                            r.primary_last, s);
-    if (st != TV_OK) break;
-    st = tv_verify_attention(d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx,
-                             L.out, L.lse, L.sel, r.row_status, L.workspace, L.workspace_bytes, s);
+  tv_status st = mask_check(d, r.parents, r.anc, r.depth, r.row_status);
+  for (int l = 0; l < n && st == TV_OK; ++l) {  // each layer as tv_verify_round runs it, the mask with layer 0
+    if ((st = layer_check(d, r, layers[l])) == TV_OK) st = layer_step(d, r, layers[l], l == 0, s);
   }
   if (st == TV_OK && r.target_logits)
     st = tv_select_accepted_path(d, r.parents, r.anc, r.depth, r.draft_tokens, r.target_logits, r.vocab,

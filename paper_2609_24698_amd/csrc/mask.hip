@@ -4,18 +4,18 @@
 // when the root has parent -1 and every other node's parent precedes it; the
 // ancestor set of node i is i plus the ancestor set of its parent (the tree
 // topology that branch-aware verification must respect, Sec. 3.1 and Sec. 4.1).
-#include "tv_common.h"
-#include "tv_internal.h"
+#include "score_h8.h"
 
 namespace tv {
 
-__global__ void __launch_bounds__(256) mask_kernel(int B, int D, const int32_t *__restrict__ parents,
-                                                   uint64_t *__restrict__ anc, int32_t *__restrict__ depth,
-                                                   int32_t *__restrict__ row_status) {
-  __shared__ int32_t par[4][64];
+// Workgroup `blk` (256 threads) takes rows 4 blk .. 4 blk + 3, one per
+// wavefront.
+__device__ __forceinline__ void mask_rows(int B, int D, const int32_t *__restrict__ parents,
+                                          uint64_t *__restrict__ anc, int32_t *__restrict__ depth,
+                                          int32_t *__restrict__ row_status, int blk, int32_t (*par)[64]) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int b = blockIdx.x * 4 + w;
+  const int b = blk * 4 + w;
   const bool live = b < B;
   const int i = lane;
   int32_t p = (live && i < D) ? parents[(int64_t)b * D + i] : 0;
@@ -40,6 +40,56 @@ __global__ void __launch_bounds__(256) mask_kernel(int B, int D, const int32_t *
     depth[(int64_t)b * D + i] = dep;
   }
   if (lane == 0) row_status[b] = row_ok ? TV_ROW_OK : TV_ROW_BAD_PARENT;
+}
+
+__global__ void __launch_bounds__(256) mask_kernel(int B, int D, const int32_t *__restrict__ parents,
+                                                   uint64_t *__restrict__ anc, int32_t *__restrict__ depth,
+                                                   int32_t *__restrict__ row_status) {
+  __shared__ int32_t par[4][64];
+  mask_rows(B, D, parents, anc, depth, row_status, blockIdx.x, par);
+}
+
+// The verify preprocess and the indexer scoring (fast path) in one launch:
+// the scoring reads only committed state and the queries, not the masks, so
+// its chunk workgroups (the scoring kernel's grid) follow the mask's in the
+// same grid.  The scoring skips no row on its status, which the mask writes
+// meanwhile; a row the mask fails gets scores that no later step reads.
+template <bool FP8>
+__global__ void __launch_bounds__(256) mask_score_kernel(tv_dims d, const int32_t *__restrict__ parents,
+                                                         uint64_t *__restrict__ anc, int32_t *__restrict__ depth,
+                                                         int32_t *__restrict__ row_status, CacheView c,
+                                                         const uint16_t *__restrict__ q_idx,
+                                                         const uint16_t *__restrict__ w_idx,
+                                                         float *__restrict__ scores, int score_stride,
+                                                         int chunks_per_row) {
+  __shared__ union {
+    int32_t par[4][64];
+    ScoreH8Smem<4> ss;
+  } sm;
+  const int nmask = (d.B + 3) / 4;
+  if ((int)blockIdx.x < nmask) {
+    mask_rows(d.B, d.D, parents, anc, depth, row_status, blockIdx.x, sm.par);
+  } else {
+    const int k = blockIdx.x - nmask, b = k / chunks_per_row;
+    score_h8_chunk<FP8, 4, false>(d, c, q_idx, w_idx, nullptr, scores, score_stride, b, k - b * chunks_per_row,
+                                  sm.ss);
+  }
+}
+
+hipError_t launch_mask_score(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
+                             int32_t *row_status, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
+                             float *scores, int32_t score_stride, hipStream_t s) {
+  if (!score_fast_path(d)) return hipErrorInvalidValue;
+  const int chunks = std::max(1, (d.max_len / d.ratio_csa + 255) / 256);
+  const int64_t grid = (int64_t)(d.B + 3) / 4 + (int64_t)d.B * chunks;
+  if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+  if (d.idx_fmt == TV_IDX_E4M3)
+    mask_score_kernel<true><<<(unsigned)grid, 256, 0, s>>>(d, parents, anc, depth, row_status, c, q_idx, w_idx,
+                                                           scores, score_stride, chunks);
+  else
+    mask_score_kernel<false><<<(unsigned)grid, 256, 0, s>>>(d, parents, anc, depth, row_status, c, q_idx, w_idx,
+                                                            scores, score_stride, chunks);
+  return hipGetLastError();
 }
 
 hipError_t launch_mask(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,

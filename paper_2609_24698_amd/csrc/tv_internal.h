@@ -79,6 +79,14 @@ hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t 
                            uint16_t *pool_c4_idx, hipStream_t s);
 hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
                         const int32_t *row_status, float *scores, int32_t score_stride, hipStream_t s);
+// The scoring's fast path (H_idx = 8, D <= 8), which launch_mask_score
+// requires.
+bool score_fast_path(const tv_dims &d);
+// launch_mask and launch_score (fast path) as one launch: the mask's
+// workgroups first, then the scoring chunks, which do not read the masks.
+hipError_t launch_mask_score(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
+                             int32_t *row_status, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
+                             float *scores, int32_t score_stride, hipStream_t s);
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,

@@ -185,3 +185,20 @@ def test_round_graph_arguments_checked_without_gpu():
     assert lib.tv_round_graph_launch(None, None) == binding.TV_ERR_INVALID_ARG
     assert lib.tv_round_graph_destroy(None) == binding.TV_ERR_INVALID_ARG
     assert lib.tv_round_graph_kernels(None) == 0
+
+
+def test_verify_round_arguments_checked_without_gpu():
+    lib = binding.lib()
+    d = _dims()
+    rnd = binding.TvRound()
+    layer = binding.TvLayer()
+    assert lib.tv_verify_round(ctypes.byref(d), None, ctypes.byref(layer), None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_verify_round(ctypes.byref(d), ctypes.byref(rnd), None, None) == binding.TV_ERR_INVALID_ARG
+    assert lib.tv_verify_round(ctypes.byref(_dims(B=0)), ctypes.byref(rnd), ctypes.byref(layer), None) == \
+        binding.TV_ERR_INVALID_ARG
+    # without parents the mask is not built, but the layer's buffers are still checked
+    assert lib.tv_verify_round(ctypes.byref(d), ctypes.byref(rnd), ctypes.byref(layer), None) == \
+        binding.TV_ERR_INVALID_ARG
+    rnd.parents, rnd.anc, rnd.depth, rnd.row_status = 1 << 20, 1 << 21, 1 << 22, 1 << 23
+    assert lib.tv_verify_round(ctypes.byref(d), ctypes.byref(rnd), ctypes.byref(layer), None) == \
+        binding.TV_ERR_INVALID_ARG  # null layer buffers

@@ -2,7 +2,9 @@
 same calls issued one by one, round after round (the committed state grows),
 with eager work and synchronisations between replays, and with new draft
 trees written into the captured buffers between replays.  Layer 0 of the
-first round is also checked against the oracle."""
+first round is also checked against the oracle.  The one-call layer step
+(tv_verify_round, indexer scoring beside the compression on a second
+stream) gives the same bits as the separate calls on one stream."""
 import sys
 
 import numpy as np
@@ -61,10 +63,10 @@ def test_graph_equals_eager(name, n, select, over):
     _, rb = _layers(name, n, select, **over)
     eager, graph = LayeredRound(ra), LayeredRound(rb)
     kernels = graph.capture()
-    assert kernels >= 1 + 4 * n + n
+    assert kernels >= 1 + 3 * n + n  # mask; per layer compression with scoring, top-k, attention; commits
     noise = torch.empty(1 << 20, device="cuda:0")
     for rnd in range(3):
-        eager.eager()
+        eager.eager(fused=False)
         graph.replay()
         torch.cuda.synchronize()
         if rnd == 0:  # layer 0 against the oracle
@@ -81,6 +83,50 @@ def test_graph_equals_eager(name, n, select, over):
         torch.cuda.synchronize()
     assert np.all(rb[0].host("len") > ws[0].lens)
     graph.release()
+
+
+@pytest.mark.parametrize("name,n,select,over", [
+    ("C1", 3, True, {}),
+    ("C2", 2, True, dict(B=4, lens=[32767, 20000, 4099, 1023])),
+    ("C4", 1, False, {}),
+    ("C3", 1, False, dict(B=16)),
+    ("C1", 2, False, dict(idx_fmt=1)),        # FP8 indexer keys
+    ("C1", 2, False, dict(page_size=256)),    # paged pool
+    ("C1", 2, False, dict(D=12)),             # beyond the scoring's fast path: compression, then scoring
+])
+def test_one_call_layer_step_equals_calls(name, n, select, over):
+    """Per layer one tv_verify_round (mask with layer 0 only) against mask,
+    compress and verify issued separately, round after round, on a stream
+    that is not the current one."""
+    from paper_2609_24698_amd import LayeredRound
+    _say(f"[one-call] {name} layers={n} select={select} {over}")
+    _, ra = _layers(name, n, select, **over)
+    _, rb = _layers(name, n, select, **over)
+    calls, fused = LayeredRound(ra), LayeredRound(rb)
+    s = torch.cuda.Stream()
+    for rnd in range(3):
+        calls.eager(fused=False)
+        with torch.cuda.stream(s):
+            fused.eager(s, fused=True)
+        torch.cuda.synchronize()
+        _same(calls, fused, rnd)
+    assert np.all(rb[0].host("row_status") == 0)
+
+
+def test_device_round_step_equals_calls():
+    """DeviceRound.round (one-call layer step, then selection and commit)
+    against round_calls, with the designated-chain refresh on."""
+    _, ra = _layers("C1", 1, True)
+    _, rb = _layers("C1", 1, True)
+    keys = PER_LAYER + SHARED
+    for r in (ra[0], rb[0]):
+        r.set_primary(r.host("accepted_last"))
+    for rnd in range(3):
+        ra[0].round_calls()
+        rb[0].round()
+        torch.cuda.synchronize()
+        for k in keys:
+            assert np.array_equal(ra[0].host(k).view(np.uint8), rb[0].host(k).view(np.uint8)), (rnd, k)
 
 
 def test_new_trees_without_recapture():
@@ -101,7 +147,7 @@ def test_new_trees_without_recapture():
         for lr in (eager, graph):
             lr.layers[0].t["parents"].copy_(torch.from_numpy(par))
             lr.layers[0].t["accepted_last"].copy_(torch.from_numpy(acc))
-        eager.eager()
+        eager.eager(fused=False)
         graph.replay()
         torch.cuda.synchronize()
         _same(eager, graph, rnd)
