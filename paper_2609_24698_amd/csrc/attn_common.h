@@ -22,9 +22,11 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // order.
 //
 // With 8 rows or more, rows are dealt to XCDs in the order row_order gives
-// (longest first): every unit of the row of rank rho runs on XCD rho % 8,
-// where the row's shared HCA, window and overlapping CSA entries stay in one
-// L2, and each XCD starts its longest rows first.
+// (longest first), back and forth: ranks 0..7 go to XCDs 0..7, ranks 8..15 to
+// XCDs 7..0, and so on, so that no XCD takes the longest row of every group
+// of eight.  Every unit of a row runs on one XCD, where the row's shared HCA,
+// window and overlapping CSA entries stay in one L2, and each XCD starts its
+// longest rows first.
 //
 // With fewer rows that would leave XCDs idle, so the (row, node, split) units
 // are dealt over all eight: consecutive units go to consecutive XCDs.  When a
@@ -46,7 +48,8 @@ __device__ __forceinline__ int unit_of(int blk, int B, int D, int splits, int &i
   s = q % splits;
   const int r = q / splits;
   i = r % D;
-  return (r / D) * 8 + x;
+  const int g = r / D;  // group of eight ranks
+  return g * 8 + ((g & 1) ? 7 - x : x);
 }
 
 // Barrier that waits for this wavefront's LDS traffic only: global loads in
