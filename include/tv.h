@@ -21,8 +21,9 @@
  *                            state; rejected branches leave no trace (Sec. 3.2,
  *                            Sec. 4.2)
  *   tv_verify_round          mask, compression and verification of one layer in
- *                            one call, the indexer scoring in the mask's launch
- *                            (Sec. 4.1, Sec. 4.3)
+ *                            one call, with fewer launches: the compression and
+ *                            the indexer scoring ride in the mask's and the
+ *                            top-k's launches (Sec. 4.1, Sec. 4.3)
  *
  * Reading of the compressed-attention arithmetic (the paper cites DeepSeek-V4
  * for it): a ratio-r entry pools the r raw rows of a block with softmax
@@ -336,7 +337,11 @@ typedef struct {
  * that order on `stream` with the same arguments.  The indexer scoring reads
  * only committed CSA keys and the indexer queries, neither the masks nor the
  * compression's output, so where its fast path applies (H_idx = 8, D <= 8)
- * it runs in the same kernel launch as the mask, one launch fewer per step
+ * it runs in the same kernel launch as the mask.  With a flat pool and CSA
+ * blocks of at most 4 tokens, the compression needs no launch of its own
+ * either: each CSA entry is pooled by one wavefront in the mask's launch
+ * (from the parent array, not the masks being written), and each HCA entry,
+ * which the top-k does not read, by a workgroup in the top-k's launch
  * (overlap of independent device work, Sec. 4.3).  Everything runs on `stream`, in order
  * with earlier and later work on it.  The selection inputs of `round`
  * (draft_tokens, target_logits, ...) and accepted_last, accept_nodes,

@@ -285,10 +285,13 @@ static tv_status verify_score(const tv_dims &d, const tv_cache *cache, const uin
 }
 
 // The rest of the verify call: selection (and merge), attention (and combine).
+// With hca_gate_w (the split compression's gate rows), the top-k launch also
+// pools the HCA entries into hca_out (the scr_c128 buffer).
 static tv_status verify_rest(const tv_dims &d, const tv_cache *cache, const uint16_t *tree_u, const uint64_t *anc,
                              const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q,
                              const uint16_t *q_idx, const uint16_t *w_idx, uint16_t *out, float *lse, int32_t *sel,
-                             int32_t *row_status, void *workspace, hipStream_t stream) {
+                             int32_t *row_status, void *workspace, hipStream_t stream,
+                             const uint16_t *hca_gate_w = nullptr, uint16_t *hca_out = nullptr) {
   const WsLayout w = ws_layout(d);
   char *ws = static_cast<char *>(workspace);
   float *scores = reinterpret_cast<float *>(ws + w.scores);
@@ -306,7 +309,8 @@ static tv_status verify_rest(const tv_dims &d, const tv_cache *cache, const uint
   int32_t *surv_cnt = reinterpret_cast<int32_t *>(ws + w.surv_cnt);
   TV_LAUNCH("topk_select", launch_topk(d, cv, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores,
                                        w.score_stride, selp, row_status, row_order, row_rank, keytab, w.plan.max_keys,
-                                       nkeys, nkeys_rank, surv_idx, surv_key, surv_cnt, stream));
+                                       nkeys, nkeys_rank, surv_idx, surv_key, surv_cnt, hca_gate_w, hca_out,
+                                       stream));
   if (topk_max_segments(d) > 1)
     TV_LAUNCH("topk_merge", launch_topk_merge(d, cv, anc, depth, scr_c4, selp, row_status, row_rank, keytab,
                                               w.plan.max_keys, surv_idx, surv_key, surv_cnt, stream));
@@ -331,32 +335,42 @@ static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const u
 }
 
 // One layer's verify preprocess (with_mask), compression and verification.
-// With the mask and the scoring's fast path, the mask and the indexer
-// scoring (which reads neither the masks nor the compression's output) are
-// one launch, then the compression, then the rest; otherwise the calls'
-// kernels in the calls' order.  Every kernel computes what it computes in the
-// separate calls, so the results are the same bits.  Arguments already
+// With the mask, the scoring's fast path, a flat pool and the split
+// compression, no kernel of its own is left for the compression: the mask's
+// launch also runs the indexer scoring (it reads neither the masks nor the
+// scratch) and the CSA entries (a wavefront per node, from the parent array),
+// and the top-k's launch also runs the HCA entries (the top-k only lists
+// their addresses).  With the mask and the scoring's fast path otherwise, the
+// mask and the scoring share a launch before the compression.  Otherwise the
+// calls' kernels in the calls' order.  Every part computes what it computes
+// in the separate calls, so the results are the same bits.  Arguments already
 // checked.
 static tv_status layer_step(const tv_dims *d, const tv_round &r, const tv_layer &L, bool with_mask,
                             hipStream_t stream) {
   const bool fused = with_mask && score_fast_path(*d);
+  const bool split = fused && d->page_size == 0 && compress_split(*d);
   if (fused) {
     const WsLayout w = ws_layout(*d);
     float *scores = reinterpret_cast<float *>(static_cast<char *>(L.workspace) + w.scores);
     TV_LAUNCH("mask_score", launch_mask_score(*d, r.parents, r.anc, r.depth, r.row_status, view(L.cache), L.q_idx,
-                                              L.w_idx, scores, w.score_stride, stream));
+                                              L.w_idx, scores, w.score_stride, split ? L.tree_u : nullptr,
+                                              split ? L.gate_w : nullptr, split ? L.scr_c4 : nullptr,
+                                              split ? r.primary_last : nullptr, split ? L.cache.c4 : nullptr,
+                                              split ? L.cache.c4_idx : nullptr, stream));
   } else if (with_mask) {
     TV_LAUNCH("tree_mask", launch_mask(*d, r.parents, r.anc, r.depth, r.row_status, stream));
   }
-  TV_LAUNCH("branch_compress", launch_compress(*d, view(L.cache), L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4,
-                                               L.scr_c128, r.row_status, r.primary_last, L.cache.c4, L.cache.c4_idx,
-                                               stream));
+  if (!split)
+    TV_LAUNCH("branch_compress", launch_compress(*d, view(L.cache), L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4,
+                                                 L.scr_c128, r.row_status, r.primary_last, L.cache.c4,
+                                                 L.cache.c4_idx, stream));
   if (!fused) {
     const tv_status st = verify_score(*d, &L.cache, L.q_idx, L.w_idx, r.row_status, L.workspace, stream);
     if (st != TV_OK) return st;
   }
   return verify_rest(*d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, L.q, L.q_idx, L.w_idx, L.out,
-                     L.lse, L.sel, r.row_status, L.workspace, stream);
+                     L.lse, L.sel, r.row_status, L.workspace, stream, split ? L.gate_w : nullptr,
+                     split ? L.scr_c128 : nullptr);
 }
 
 static tv_status layer_check(const tv_dims *d, const tv_round &r, const tv_layer &L) {

@@ -7,19 +7,21 @@
 // acceptance (Sec. 4.1 chains compressed independently after branching;
 // Sec. 4.2 scratch pad for temporary branch state).
 //
-// One 1024-thread workgroup per (row, node); nodes that close no block exit at
-// once.  A node that closes only a short block (at most kWaveMaxR tokens, the
-// CSA block of every supported ratio) is pooled by its first wavefront alone:
-// lane k holds channel chunk k (and k + 64) of every token, so the gate
-// logits are one butterfly per token and the weighted sums stay in the lane,
-// with no workgroup barrier and no second read of the rows.  A node that closes both a CSA and an HCA block pools suffixes of the
-// same token range (both blocks end at its position), so each token row is
-// read once for the gate logits of both and once for both weighted sums.
-// The rows (committed ones from the ring, path ones from tree_u) are resolved
-// once into an LDS pointer table; gate logits (8 lanes per token, a 128-token
-// block in one pass) and the weighted sums (8 token groups per 16-byte channel
-// chunk) stream them with 16-byte loads, all of a thread's loads in flight
-// together.
+// When a CSA block fits one wavefront (ratio_csa <= kWaveMaxR, the supported
+// shapes' CSA ratio 4), compression is split (compress_body.h): a
+// wavefront per node pools the node's CSA entry (lane k holds channel chunk k
+// and k + 64 of every token, so the gate logits are one butterfly per token
+// and the weighted sums stay in the lane, with no barrier and no second read),
+// and a 512-thread workgroup per node pools its HCA entry, if it closes one;
+// the one-call layer step runs the two parts in the launches of the verify
+// preprocess and of the top-k.  Otherwise one 1024-thread workgroup per
+// (row, node) pools both blocks (nodes that close nothing exit at once): they
+// are suffixes of the same token range (both end at the node's position), so
+// each token row is read once for the gate logits of both and once for both
+// weighted sums.  The rows (committed ones from the ring, path ones from
+// tree_u) are resolved once into an LDS pointer table; gate logits (8 lanes
+// per token) and the weighted sums (token groups per 16-byte channel chunk)
+// stream them with 16-byte loads, all of a thread's loads in flight together.
 //
 // Committed rows come from the ring or, with a paged pool, from the raw
 // layer through the row's page table; a block whose committed rows lie in a
@@ -34,130 +36,11 @@
 // straight into their persistent pool slots.  Those slots lie past the
 // committed entries, so nothing reads them before the commit makes them
 // committed, and the commit then skips their copies.
-#include "pool_addr.h"
+#include "compress_body.h"
 
 namespace tv {
 
-constexpr int kMaxRatio = 1024;
-constexpr int kMaxDu = 640;       // raw row width bound (d_row + d_idx): the supported shapes' 640 and 320
-constexpr int kMaxCh = kMaxDu / 8;  // 16-byte chunks of the widest row
 constexpr int kNT = 1024;           // threads per workgroup
-constexpr int kMaxGroups = 16;      // token groups of the weighted sums
-constexpr int kWaveMaxR = 4;        // blocks of at most this many tokens are pooled by one wavefront
-
-__device__ __forceinline__ float dot8(const float *g, uint4 v) {
-  return g[0] * bf2f_lo(v.x) + g[1] * bf2f_hi(v.x) + g[2] * bf2f_lo(v.y) + g[3] * bf2f_hi(v.y) +
-         g[4] * bf2f_lo(v.z) + g[5] * bf2f_hi(v.z) + g[6] * bf2f_lo(v.w) + g[7] * bf2f_hi(v.w);
-}
-
-// The short-block path (wavefront 0 only; see above).  q0 is the block's
-// first position, m the node's ancestor mask, dj the depth of node `lane`.
-__device__ void compress_short(const tv_dims &d, const CacheView &c, const uint16_t *__restrict__ tree_u,
-                               const uint16_t *__restrict__ gate_w, int b, int64_t node, int32_t L, int64_t q0, int R,
-                               uint64_t m, int32_t dj, int32_t *path, uint16_t *__restrict__ scr_c4,
-                               int32_t *__restrict__ row_status, int64_t pslot, uint16_t *__restrict__ pool_c4,
-                               uint16_t *__restrict__ pool_c4_idx) {
-  const int lane = threadIdx.x & 63;
-  const int d_u = d.d_row + d.d_idx, nch = d_u / 8;
-  if (lane < d.D && ((m >> lane) & 1ull)) path[dj] = lane;
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the path is in LDS for the whole wave
-  __builtin_amdgcn_wave_barrier();
-  // token rows: lane t < R resolves token t, then every lane takes them by shuffle
-  const int64_t qt = q0 + (lane < R ? lane : 0);
-  int64_t ri = 0;
-  const uint16_t *rp = nullptr;
-  if (qt < L) {
-    ri = raw_index(d, c.page_table, b, qt);
-    rp = c.ring + (ri < 0 ? 0 : ri) * d_u;
-  } else {
-    rp = tree_u + ((int64_t)b * d.D + path[qt - L]) * d_u;
-  }
-  if (__any(lane < R && ri < 0)) {  // a committed row whose page is not allocated
-    if (lane == 0) row_status[b] = TV_ROW_CAPACITY;
-    return;
-  }
-  const uintptr_t rpi = reinterpret_cast<uintptr_t>(rp);
-  uint4 v[kWaveMaxR][2], g[2];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int k = lane + 64 * u;
-    g[u] = k < nch ? reinterpret_cast<const uint4 *>(gate_w)[k] : make_uint4(0, 0, 0, 0);
-  }
-#pragma unroll
-  for (int t = 0; t < kWaveMaxR; ++t) {
-    const uintptr_t rt = (uintptr_t)__shfl((unsigned long long)rpi, t < R ? t : 0, 64);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int k = lane + 64 * u;
-      v[t][u] = (t < R && k < nch) ? reinterpret_cast<const uint4 *>(rt)[k] : make_uint4(0, 0, 0, 0);
-    }
-  }
-  // gate logits: the lane's chunks of every token, then a butterfly per token
-  float gf[2][8];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    gf[u][0] = bf2f_lo(g[u].x); gf[u][1] = bf2f_hi(g[u].x);
-    gf[u][2] = bf2f_lo(g[u].y); gf[u][3] = bf2f_hi(g[u].y);
-    gf[u][4] = bf2f_lo(g[u].z); gf[u][5] = bf2f_hi(g[u].z);
-    gf[u][6] = bf2f_lo(g[u].w); gf[u][7] = bf2f_hi(g[u].w);
-  }
-  float w[kWaveMaxR];
-  float mx = -INFINITY;
-#pragma unroll
-  for (int t = 0; t < kWaveMaxR; ++t) {
-    float a = 0.f;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) a += dot8(gf[u], v[t][u]);
-    a = wave_sum(a);
-    w[t] = t < R ? a : -INFINITY;
-    mx = fmaxf(mx, w[t]);
-  }
-  float sum = 0.f;
-#pragma unroll
-  for (int t = 0; t < kWaveMaxR; ++t) {
-    w[t] = t < R ? __expf(w[t] - mx) : 0.f;
-    sum += w[t];
-  }
-  const float inv = 1.0f / sum;
-  // weighted sums of the lane's chunks, in token order
-  uint16_t *dst = scr_c4 + node * d_u;
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int k = lane + 64 * u;
-    if (k >= nch) continue;
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int t = 0; t < kWaveMaxR; ++t) {
-      if (t >= R) continue;
-      const float wt = w[t] * inv;
-      acc[0] += wt * bf2f_lo(v[t][u].x);
-      acc[1] += wt * bf2f_hi(v[t][u].x);
-      acc[2] += wt * bf2f_lo(v[t][u].y);
-      acc[3] += wt * bf2f_hi(v[t][u].y);
-      acc[4] += wt * bf2f_lo(v[t][u].z);
-      acc[5] += wt * bf2f_hi(v[t][u].z);
-      acc[6] += wt * bf2f_lo(v[t][u].w);
-      acc[7] += wt * bf2f_hi(v[t][u].w);
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int ch = 8 * k + e;
-      // FP8 indexer keys: the indexer channels of a CSA entry are E4M3 values
-      const bool fp8 = ch >= d.d_row && d.idx_fmt == TV_IDX_E4M3;
-      const uint32_t code = fp8 ? f32_to_e4m3(acc[e]) : 0u;
-      const uint16_t val = fp8 ? (uint16_t)e4m3_to_bf16(code) : f2bf(acc[e]);
-      dst[ch] = val;
-      if (pslot >= 0) {
-        if (ch < d.d_row)
-          pool_c4[pslot * d.d_row + ch] = val;
-        else if (fp8)
-          reinterpret_cast<uint8_t *>(pool_c4_idx)[pslot * d.d_idx + (ch - d.d_row)] = (uint8_t)code;
-        else
-          pool_c4_idx[pslot * d.d_idx + (ch - d.d_row)] = val;
-      }
-    }
-  }
-}
 
 __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
                                                        const uint64_t *__restrict__ anc,
@@ -209,18 +92,6 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   const int R = std::max(cl[0] ? rat[0] : 0, cl[1] ? rat[1] : 0);
   const int first[2] = {R - rat[0], R - rat[1]};
   const int64_t slot4 = (p + 1) / d.ratio_csa - 1;
-  if (!cl[1] && R <= kWaveMaxR && d_u / 8 <= 128) {  // the short-block path: wavefront 0 alone
-    if (wv != 0) return;
-    // a CSA entry closed on the designated chain also goes to its pool slot, capacity permitting
-    const uint64_t chain = (P >= 0 && P < d.D) ? __shfl(aj, P, 64) : 0ull;
-    int64_t pslot = -1;
-    if ((chain >> i) & 1ull)
-      pslot = flat ? (slot4 < cap4 ? base4 + slot4 : -1)
-                   : pool_slot(d, c.page_table, nullptr, nullptr, b, slot4, d.ratio_csa);
-    compress_short(d, c, tree_u, gate_w, b, node, L, p - R + 1, R, m, dj, path, scr_c4, row_status, pslot, pool_c4,
-                   pool_c4_idx);
-    return;
-  }
   if (tid < d.D && ((m >> tid) & 1ull)) path[dj] = tid;
   if (wv == 0) {  // the designated chain: ancestor mask of node P (lane P holds it), empty if none
     const uint64_t ap = __shfl(aj, (P >= 0 && P < d.D) ? P : 0, 64);
@@ -378,11 +249,42 @@ __global__ void __launch_bounds__(kNT) compress_kernel(tv_dims d, CacheView c, c
   }
 }
 
+// Split compression (compress_split(d)): one kHcaNT-thread workgroup per
+// node for its HCA entry (the rest exit at once), then one workgroup per
+// eight nodes, a wavefront per node, for the CSA entries.
+constexpr int kSplitWaves = kHcaNT / 64;
+__global__ void __launch_bounds__(kHcaNT) compress_split_kernel(
+    tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
+    const int32_t *__restrict__ depth, const uint16_t *__restrict__ gate_w, uint16_t *__restrict__ scr_c4,
+    uint16_t *__restrict__ scr_c128, int32_t *__restrict__ row_status, const int32_t *__restrict__ primary_last,
+    uint16_t *__restrict__ pool_c4, uint16_t *__restrict__ pool_c4_idx) {
+  __shared__ union {
+    HcaSmem h;
+    int32_t paths[kSplitWaves][64];
+  } sm;
+  const int nodes = d.B * d.D;
+  const int blk = blockIdx.x;
+  if (blk < nodes) {
+    hca_node(d, c, tree_u, anc, depth, gate_w, scr_c128, row_status, true, blk, sm.h);
+  } else {
+    const int wv = threadIdx.x >> 6, n = (blk - nodes) * kSplitWaves + wv;
+    if (n < nodes)
+      csa_wave_node<false>(d, c, nullptr, anc, depth, tree_u, gate_w, scr_c4, row_status, primary_last, pool_c4,
+                           pool_c4_idx, n, sm.paths[wv]);
+  }
+}
+
 hipError_t launch_compress(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                            const int32_t *depth, const uint16_t *gate_w, uint16_t *scr_c4, uint16_t *scr_c128,
                            int32_t *row_status, const int32_t *primary_last, uint16_t *pool_c4,
                            uint16_t *pool_c4_idx, hipStream_t s) {
   if (d.d_row + d.d_idx > kMaxDu) return hipErrorInvalidValue;
+  if (compress_split(d)) {
+    const int nodes = d.B * d.D;
+    compress_split_kernel<<<nodes + (nodes + kSplitWaves - 1) / kSplitWaves, kHcaNT, 0, s>>>(
+        d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status, primary_last, pool_c4, pool_c4_idx);
+    return hipGetLastError();
+  }
   dim3 grid(d.B * d.D);
   compress_kernel<<<grid, kNT, 0, s>>>(d, c, tree_u, anc, depth, gate_w, scr_c4, scr_c128, row_status, primary_last,
                                        pool_c4, pool_c4_idx);

@@ -26,6 +26,7 @@
 // count are kept by (row rank, node), the attention's own order.
 #include <algorithm>
 
+#include "compress_body.h"
 #include "node_keys.h"
 #include "tv_common.h"
 #include "tv_internal.h"
@@ -248,28 +249,32 @@ __device__ __forceinline__ int topk_segments(int n4) { return n4 <= kTopkSeg ? 1
 // One workgroup per (node, segment).  Segment 0 of node 0 of a row also ranks
 // the row by length for the attention's row order, and segment 0 of every
 // node writes the node's non-CSA keys into its key table.
-__global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4))) topk_kernel(tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u,
-                                                     const uint64_t *__restrict__ anc,
-                                                     const int32_t *__restrict__ depth,
-                                                     const uint16_t *__restrict__ scr_c4,
-                                                     const uint16_t *__restrict__ scr_c128,
-                                                     const uint16_t *__restrict__ q_idx,
-                                                     const uint16_t *__restrict__ w_idx,
-                                                     const float *__restrict__ scores, int score_stride,
-                                                     int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
-                                                     int32_t *__restrict__ row_order, int32_t *__restrict__ row_rank,
-                                                     const uint16_t **__restrict__ keytab, int keytab_stride,
-                                                     int32_t *__restrict__ nkeys_tab, int32_t *__restrict__ nkeys_rank,
-                                                     int max_seg,
-                                                     int32_t *__restrict__ surv_idx, uint32_t *__restrict__ surv_key,
-                                                     int32_t *__restrict__ surv_cnt) {
-  __shared__ SelShared sh;
-  __shared__ float scr_score[kMaxScratch];
-  __shared__ int wcnt[kTkNW];
-  __shared__ int32_t path[64], hca_node[64];
+struct TopkSmem {
+  SelShared sh;
+  float scr_score[kMaxScratch];
+  int wcnt[kTkNW];
+  int32_t path[64], hca_nd[64];
+};
+
+__device__ __forceinline__ void topk_node(const tv_dims &d, const CacheView &c, const uint16_t *__restrict__ tree_u,
+                                          const uint64_t *__restrict__ anc, const int32_t *__restrict__ depth,
+                                          const uint16_t *__restrict__ scr_c4, const uint16_t *__restrict__ scr_c128,
+                                          const uint16_t *__restrict__ q_idx, const uint16_t *__restrict__ w_idx,
+                                          const float *__restrict__ scores, int score_stride,
+                                          int32_t *__restrict__ sel, int32_t *__restrict__ row_status,
+                                          int32_t *__restrict__ row_order, int32_t *__restrict__ row_rank,
+                                          const uint16_t **__restrict__ keytab, int keytab_stride,
+                                          int32_t *__restrict__ nkeys_tab, int32_t *__restrict__ nkeys_rank,
+                                          int max_seg, int32_t *__restrict__ surv_idx,
+                                          uint32_t *__restrict__ surv_key, int32_t *__restrict__ surv_cnt, int blk,
+                                          TopkSmem &sm) {
+  SelShared &sh = sm.sh;
+  float *scr_score = sm.scr_score;
+  int *wcnt = sm.wcnt;
+  int32_t *path = sm.path, *hca_nd = sm.hca_nd;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t node = blockIdx.x / max_seg;
-  const int seg = blockIdx.x - (int)node * max_seg;
+  const int64_t node = blk / max_seg;
+  const int seg = blk - (int)node * max_seg;
   const int b = (int)(node / d.D);
   const int i = (int)(node - (int64_t)b * d.D);
   // one round trip: everything whose address is known from (row, node, lane)
@@ -335,7 +340,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
 
   // The node's root path (its key layout) from the ancestor mask, no barrier.
   uint64_t csa_mask;
-  const NodeKeys nk = path_keys(d, L, i, m, dl, path, hca_node, csa_mask);
+  const NodeKeys nk = path_keys(d, L, i, m, dl, path, hca_nd, csa_mask);
 
   // Entries closed on the root path take the consecutive logical indices
   // n4, n4+1, ... in depth (= node index) order; the last segment scores them.
@@ -370,7 +375,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
       if (lane == 0) scr_score[t] = sum;
     }
   }
-  lds_barrier();  // path, hca_node, the path-entry scores and the wave counts of the rank are visible
+  lds_barrier();  // path, hca_nd, the path-entry scores and the wave counts of the rank are visible
   const int64_t rnode = (int64_t)rank_of_row() * d.D + i;
   const int seg_n = cn + nscr;  // path entries follow the committed ones of the last segment
 #pragma unroll
@@ -385,7 +390,7 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
   const uint16_t **tab = keytab + rnode * keytab_stride;
   if (seg == 0) {
     for (int t = nk.nsel + tid; t < nk.n_keys; t += kTkNT)
-      tab[t] = key_row(d, nk, b, t, nullptr, path, hca_node, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128,
+      tab[t] = key_row(d, nk, b, t, nullptr, path, hca_nd, c.ring, c.c4, c4b, c.c128, c128b, scr_c4, scr_c128,
                        tree_u, c.page_table);
     if (tid == 0) {
       nkeys_tab[node] = nk.n_keys;
@@ -424,6 +429,48 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
     }
     if (tid == 0) surv_cnt[node * max_seg + seg] = taken;
   }
+}
+
+
+__global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4))) topk_kernel(
+    tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
+    const int32_t *__restrict__ depth, const uint16_t *__restrict__ scr_c4, const uint16_t *__restrict__ scr_c128,
+    const uint16_t *__restrict__ q_idx, const uint16_t *__restrict__ w_idx, const float *__restrict__ scores,
+    int score_stride, int32_t *__restrict__ sel, int32_t *__restrict__ row_status, int32_t *__restrict__ row_order,
+    int32_t *__restrict__ row_rank, const uint16_t **__restrict__ keytab, int keytab_stride,
+    int32_t *__restrict__ nkeys_tab, int32_t *__restrict__ nkeys_rank, int max_seg, int32_t *__restrict__ surv_idx,
+    uint32_t *__restrict__ surv_key, int32_t *__restrict__ surv_cnt) {
+  __shared__ TopkSmem sm;
+  topk_node(d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores, score_stride, sel, row_status,
+            row_order, row_rank, keytab, keytab_stride, nkeys_tab, nkeys_rank, max_seg, surv_idx, surv_key, surv_cnt,
+            blockIdx.x, sm);
+}
+
+// The top-k and, in the same grid after its workgroups, the HCA entries of
+// the split compression (one workgroup per node; nodes that close no HCA
+// block exit at once).  The top-k reads no HCA scratch entry (it only lists
+// their addresses), so the two are independent; the HCA workgroups start as
+// the short nodes' selections finish.
+__global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4))) topk_hca_kernel(
+    tv_dims d, CacheView c, const uint16_t *__restrict__ tree_u, const uint64_t *__restrict__ anc,
+    const int32_t *__restrict__ depth, const uint16_t *__restrict__ scr_c4, uint16_t *__restrict__ scr_c128,
+    const uint16_t *__restrict__ q_idx, const uint16_t *__restrict__ w_idx, const float *__restrict__ scores,
+    int score_stride, int32_t *__restrict__ sel, int32_t *__restrict__ row_status, int32_t *__restrict__ row_order,
+    int32_t *__restrict__ row_rank, const uint16_t **__restrict__ keytab, int keytab_stride,
+    int32_t *__restrict__ nkeys_tab, int32_t *__restrict__ nkeys_rank, int max_seg, int32_t *__restrict__ surv_idx,
+    uint32_t *__restrict__ surv_key, int32_t *__restrict__ surv_cnt, const uint16_t *__restrict__ gate_w) {
+  static_assert(kTkNT == kHcaNT, "one workgroup size for both roles");
+  __shared__ union {
+    TopkSmem t;
+    HcaSmem h;
+  } sm;
+  const int ntk = d.B * d.D * max_seg;
+  if ((int)blockIdx.x < ntk)
+    topk_node(d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores, score_stride, sel, row_status,
+              row_order, row_rank, keytab, keytab_stride, nkeys_tab, nkeys_rank, max_seg, surv_idx, surv_key,
+              surv_cnt, blockIdx.x, sm.t);
+  else
+    hca_node(d, c, tree_u, anc, depth, gate_w, scr_c128, row_status, false, blockIdx.x - ntk, sm.h);
 }
 
 // Merge of a segmented node: the topk of the survivors of all its segments.
@@ -514,10 +561,22 @@ hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tre
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
                        int32_t *row_status, int32_t *row_order, int32_t *row_rank, const uint16_t **keytab,
                        int32_t keytab_stride, int32_t *nkeys, int32_t *nkeys_rank, int32_t *surv_idx,
-                       uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s) {
+                       uint32_t *surv_key, int32_t *surv_cnt, const uint16_t *hca_gate_w, uint16_t *hca_out,
+                       hipStream_t s) {
   if (d.D > kMaxScratch || !topk_supported(d)) return hipErrorInvalidValue;
   const int max_seg = topk_max_segments(d);
-  topk_kernel<<<(unsigned)((int64_t)d.B * d.D * max_seg), kTkNT, 0, s>>>(
+  const int64_t ntk = (int64_t)d.B * d.D * max_seg;
+  if (hca_gate_w) {  // with the HCA entries of the split compression, into hca_out (the scr_c128 buffer)
+    if (!compress_split(d) || d.d_row + d.d_idx > kMaxDu || hca_out != scr_c128 ||
+        ntk + (int64_t)d.B * d.D > 0x7FFFFFFF)
+      return hipErrorInvalidValue;
+    topk_hca_kernel<<<(unsigned)(ntk + (int64_t)d.B * d.D), kTkNT, 0, s>>>(
+        d, c, tree_u, anc, depth, scr_c4, hca_out, q_idx, w_idx, scores, score_stride, sel,
+        row_status, row_order, row_rank, keytab, keytab_stride, nkeys, nkeys_rank, max_seg, surv_idx, surv_key,
+        surv_cnt, hca_gate_w);
+    return hipGetLastError();
+  }
+  topk_kernel<<<(unsigned)ntk, kTkNT, 0, s>>>(
       d, c, tree_u, anc, depth, scr_c4, scr_c128, q_idx, w_idx, scores, score_stride, sel, row_status, row_order,
       row_rank, keytab, keytab_stride, nkeys, nkeys_rank, max_seg, surv_idx, surv_key, surv_cnt);
   return hipGetLastError();

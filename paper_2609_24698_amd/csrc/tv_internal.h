@@ -59,6 +59,14 @@ struct WsLayout {
 
 SplitPlan split_plan(const tv_dims &d);
 
+// Compression blocks of at most this many tokens are pooled by one wavefront.
+constexpr int kWaveMaxR = 4;
+// Split compression applies: a CSA block fits one wavefront's registers, so
+// CSA and HCA entries are pooled by separate workgroups.
+__host__ __device__ inline bool compress_split(const tv_dims &d) {
+  return d.ratio_csa <= kWaveMaxR && (d.d_row + d.d_idx) / 8 <= 128;
+}
+
 // Splits per node as the attention grid lays them out: with fewer than 8
 // rows and 8 splits or more, padded to a multiple of 8 (split s on XCD s % 8).
 __host__ __device__ inline int attn_padded_splits(int B, int splits) {
@@ -83,16 +91,25 @@ hipError_t launch_score(const tv_dims &d, const CacheView &c, const uint16_t *q_
 // requires.
 bool score_fast_path(const tv_dims &d);
 // launch_mask and launch_score (fast path) as one launch: the mask's
-// workgroups first, then the scoring chunks, which do not read the masks.
+// workgroups first, then the scoring chunks, which do not read the masks;
+// the mask also fails a valid tree whose length is out of range.  With
+// csa_gate_w not NULL (split compression, flat pool), the launch also pools
+// every CSA entry the tree closes into csa_scr_c4 (and the designated chain's
+// into the pool), as the compression does.
 hipError_t launch_mask_score(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
                              int32_t *row_status, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
-                             float *scores, int32_t score_stride, hipStream_t s);
+                             float *scores, int32_t score_stride, const uint16_t *csa_tree_u,
+                             const uint16_t *csa_gate_w, uint16_t *csa_scr_c4, const int32_t *csa_primary_last,
+                             uint16_t *csa_pool_c4, uint16_t *csa_pool_c4_idx, hipStream_t s);
+// With hca_gate_w not NULL (split compression only), the launch also pools
+// every HCA entry the tree closes into hca_out, which must be scr_c128.
 hipError_t launch_topk(const tv_dims &d, const CacheView &c, const uint16_t *tree_u, const uint64_t *anc,
                        const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128, const uint16_t *q_idx,
                        const uint16_t *w_idx, const float *scores, int32_t score_stride, int32_t *sel,
                        int32_t *row_status, int32_t *row_order, int32_t *row_rank, const uint16_t **keytab,
                        int32_t keytab_stride, int32_t *nkeys, int32_t *nkeys_rank, int32_t *surv_idx,
-                       uint32_t *surv_key, int32_t *surv_cnt, hipStream_t s);
+                       uint32_t *surv_key, int32_t *surv_cnt, const uint16_t *hca_gate_w, uint16_t *hca_out,
+                       hipStream_t s);
 hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_t *anc, const int32_t *depth,
                              const uint16_t *scr_c4, int32_t *sel, const int32_t *row_status,
                              const int32_t *row_rank, const uint16_t **keytab, int32_t keytab_stride,

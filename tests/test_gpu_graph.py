@@ -93,6 +93,7 @@ def test_graph_equals_eager(name, n, select, over):
     ("C1", 2, False, dict(idx_fmt=1)),        # FP8 indexer keys
     ("C1", 2, False, dict(page_size=256)),    # paged pool
     ("C1", 2, False, dict(D=12)),             # beyond the scoring's fast path: compression, then scoring
+    ("C1", 2, True, dict(lens=[128 * (k + 8) - 1 - (k % 6) for k in range(8)])),  # an HCA block at every depth
 ])
 def test_one_call_layer_step_equals_calls(name, n, select, over):
     """Per layer one tv_verify_round (mask with layer 0 only) against mask,
