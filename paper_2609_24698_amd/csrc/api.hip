@@ -335,24 +335,25 @@ static tv_status verify_impl(const tv_dims *dims, const tv_cache *cache, const u
 }
 
 // One layer's verify preprocess (with_mask), compression and verification.
-// With the mask, the scoring's fast path, a flat pool and the split
-// compression, no kernel of its own is left for the compression: the mask's
-// launch also runs the indexer scoring (it reads neither the masks nor the
-// scratch) and the CSA entries (a wavefront per node, from the parent array),
-// and the top-k's launch also runs the HCA entries (the top-k only lists
-// their addresses).  With the mask and the scoring's fast path otherwise, the
-// mask and the scoring share a launch before the compression.  Otherwise the
-// calls' kernels in the calls' order.  Every part computes what it computes
+// With the scoring's fast path, a flat pool and the split compression, no
+// kernel of its own is left for the compression: the first launch runs the
+// mask (with_mask), the CSA entries (a wavefront per node; beside the mask
+// from the parent array) and the indexer scoring (it reads neither the masks
+// nor the scratch), and the top-k's launch also runs the HCA entries (the
+// top-k only lists their addresses).  With the mask and the scoring's fast
+// path otherwise, the mask and the scoring share a launch before the
+// compression.  Otherwise the calls' kernels in the calls' order.  Every part computes what it computes
 // in the separate calls, so the results are the same bits.  Arguments already
 // checked.
 static tv_status layer_step(const tv_dims *d, const tv_round &r, const tv_layer &L, bool with_mask,
                             hipStream_t stream) {
-  const bool fused = with_mask && score_fast_path(*d);
-  const bool split = fused && d->page_size == 0 && compress_split(*d);
+  const bool split = score_fast_path(*d) && d->page_size == 0 && compress_split(*d);
+  const bool fused = (with_mask && score_fast_path(*d)) || split;
   if (fused) {
     const WsLayout w = ws_layout(*d);
     float *scores = reinterpret_cast<float *>(static_cast<char *>(L.workspace) + w.scores);
-    TV_LAUNCH("mask_score", launch_mask_score(*d, r.parents, r.anc, r.depth, r.row_status, view(L.cache), L.q_idx,
+    TV_LAUNCH("mask_score", launch_mask_score(*d, with_mask ? r.parents : nullptr, r.anc, r.depth, r.row_status,
+                                              view(L.cache), L.q_idx,
                                               L.w_idx, scores, w.score_stride, split ? L.tree_u : nullptr,
                                               split ? L.gate_w : nullptr, split ? L.scr_c4 : nullptr,
                                               split ? r.primary_last : nullptr, split ? L.cache.c4 : nullptr,

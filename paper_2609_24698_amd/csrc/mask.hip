@@ -61,7 +61,10 @@ __global__ void __launch_bounds__(256) mask_kernel(int B, int D, const int32_t *
 // meanwhile; a row the mask fails gets scores that no later step reads.
 // With the split compression's CSA entries (csa.gate_w not NULL), a
 // wavefront per node pools them between the two, deriving the node's
-// ancestors from the parent array itself (csa_wave_node<true>).
+// ancestors from the parent array itself (csa_wave_node<true>).  Without
+// parents the launch has no mask workgroups: the masks and the row status
+// are already final (a later layer of the round), and the CSA wavefronts
+// read them.
 struct CsaArgs {
   const uint16_t *tree_u, *gate_w;
   uint16_t *scr_c4;
@@ -82,15 +85,20 @@ __global__ void __launch_bounds__(256) mask_score_kernel(tv_dims d, const int32_
     int32_t paths[4][64];
     ScoreH8Smem<4> ss;
   } sm;
-  const int nmask = (d.B + 3) / 4;
+  const int nmask = parents ? (d.B + 3) / 4 : 0;
   const int blk = blockIdx.x;
   if (blk < nmask) {
     mask_rows(d.B, d.D, parents, anc, depth, row_status, c.len, d.max_len, blk, sm.par);
   } else if (blk < nmask + ncsa) {
     const int wv = threadIdx.x >> 6, n = (blk - nmask) * 4 + wv;
-    if (n < d.B * d.D)
-      csa_wave_node<true>(d, c, parents, nullptr, nullptr, csa.tree_u, csa.gate_w, csa.scr_c4, row_status,
-                          csa.primary_last, csa.pool_c4, csa.pool_c4_idx, n, sm.paths[wv]);
+    if (n < d.B * d.D) {
+      if (parents)  // beside the mask: ancestors from the parent array
+        csa_wave_node<true>(d, c, parents, nullptr, nullptr, csa.tree_u, csa.gate_w, csa.scr_c4, row_status,
+                            csa.primary_last, csa.pool_c4, csa.pool_c4_idx, n, sm.paths[wv]);
+      else  // the masks and row status are final
+        csa_wave_node<false>(d, c, nullptr, anc, depth, csa.tree_u, csa.gate_w, csa.scr_c4, row_status,
+                             csa.primary_last, csa.pool_c4, csa.pool_c4_idx, n, sm.paths[wv]);
+    }
   } else {
     const int k = blk - nmask - ncsa, b = k / chunks_per_row;
     score_h8_chunk<FP8, 4, false>(d, c, q_idx, w_idx, nullptr, scores, score_stride, b, k - b * chunks_per_row,
@@ -108,7 +116,7 @@ hipError_t launch_mask_score(const tv_dims &d, const int32_t *parents, uint64_t 
   if (with_csa && (!compress_split(d) || d.page_size != 0)) return hipErrorInvalidValue;
   const int chunks = std::max(1, (d.max_len / d.ratio_csa + 255) / 256);
   const int ncsa = with_csa ? (d.B * d.D + 3) / 4 : 0;
-  const int64_t grid = (int64_t)(d.B + 3) / 4 + ncsa + (int64_t)d.B * chunks;
+  const int64_t grid = (parents ? (int64_t)(d.B + 3) / 4 : 0) + ncsa + (int64_t)d.B * chunks;
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
   const CsaArgs csa{csa_tree_u, csa_gate_w, csa_scr_c4, csa_primary_last, csa_pool_c4, csa_pool_c4_idx};
   if (d.idx_fmt == TV_IDX_E4M3)

@@ -95,7 +95,8 @@ bool score_fast_path(const tv_dims &d);
 // the mask also fails a valid tree whose length is out of range.  With
 // csa_gate_w not NULL (split compression, flat pool), the launch also pools
 // every CSA entry the tree closes into csa_scr_c4 (and the designated chain's
-// into the pool), as the compression does.
+// into the pool), as the compression does.  With parents NULL there is no
+// mask: anc, depth and row_status are inputs.
 hipError_t launch_mask_score(const tv_dims &d, const int32_t *parents, uint64_t *anc, int32_t *depth,
                              int32_t *row_status, const CacheView &c, const uint16_t *q_idx, const uint16_t *w_idx,
                              float *scores, int32_t score_stride, const uint16_t *csa_tree_u,
