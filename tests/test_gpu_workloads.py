@@ -222,6 +222,29 @@ def test_row_errors():
     _check_stages(w, ref, r, rerun=_rerun(w, ref))
 
 
+def test_row_errors_one_call():
+    """The same row errors through the one-call layer step (mask, CSA entries
+    and scoring in one launch, HCA entries in the top-k's): every output, the
+    cache and the row status equal the separate calls' bit for bit, two
+    rounds in a row."""
+    w = _small()
+    w.parents[1, 3] = 5
+    w.accepted_last[2] = w.D
+    w.c4_cap[3] = int(w.lens[3]) // 4
+    w.lens[4] = w.dims["max_len"] + 1
+    ra, rb = _device(w), _device(w)
+    keys = ("out", "lse", "sel", "scr_c4", "scr_c128", "anc", "depth", "row_status", "accept_nodes", "accept_len",
+            "ring", "c4", "c4_idx", "c128", "len")
+    for rnd in range(2):
+        ra.round_calls()
+        rb.round()
+        torch.cuda.synchronize()
+        for k in keys:
+            assert np.array_equal(ra.host(k).view(np.uint8), rb.host(k).view(np.uint8)), (rnd, k)
+    assert list(rb.host("row_status")) == [O.ROW_OK, O.ROW_BAD_PARENT, O.ROW_BAD_ACCEPT, O.ROW_CAPACITY,
+                                           O.ROW_BAD_LEN]
+
+
 def test_deterministic():
     """Two launches on the same inputs give the same bits (fixed reduction orders)."""
     w = _small(seed=72)
