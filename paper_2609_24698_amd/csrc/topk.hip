@@ -35,6 +35,7 @@ namespace tv {
 
 constexpr int kMaxScratch = 64;
 constexpr int kTkNT = 512;  // threads of a selecting workgroup
+constexpr int kMergeNT = 1024;  // threads of a merging workgroup (one per node: the more, the fewer keys each)
 constexpr int kTkNW = kTkNT / 64;
 constexpr int kTkKPT = 34;  // keys per thread of a segment: kTopkSeg committed entries plus up to 64 path entries
 constexpr int kTkBits = 13, kTkBins = 1 << kTkBits;
@@ -43,7 +44,7 @@ static_assert(kTkNT * kTopkMergeKPT == kTopkMergeCap, "merge capacity");
 
 struct __align__(16) SelShared {
   uint32_t hist[kTkBins];
-  int wsum[kTkNW];
+  int wsum[16];  // one per wavefront of the largest workgroup (1024 threads)
   int found[3];
   uint32_t bits[2][16 * kTopkMergeKPT];  // compaction bitmaps in element order: keys above the threshold, equal to it
 };
@@ -70,10 +71,11 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b) {
 // every thread has prefix, pmask and remaining such that the k largest are the
 // keys with (key & pmask) > prefix and the `remaining` lowest elements with
 // (key & pmask) == prefix.
-template <int KPT>
+template <int KPT, int NT = kTkNT>
 __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int n, int k, SelShared &sh,
                                                 uint32_t &prefix, uint32_t &pmask, int &remaining) {
-  const int nr = (n + kTkNT - 1) / kTkNT;  // slots that hold any element below n
+  static_assert(NT % 64 == 0 && NT / 64 <= 16 && 16 * NT >= kTkBins, "wave sums and the scan's bins fit");
+  const int nr = (n + NT - 1) / NT;  // slots that hold any element below n
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   prefix = 0;
   pmask = 0;
@@ -85,7 +87,7 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
     const int sft = shift - nb;
     const int nbins = 1 << nb;
     const uint32_t dmask = (uint32_t)nbins - 1u;
-    for (int t = tid; t < nbins / 4; t += kTkNT) reinterpret_cast<uint4 *>(sh.hist)[t] = make_uint4(0, 0, 0, 0);
+    for (int t = tid; t < nbins / 4; t += NT) reinterpret_cast<uint4 *>(sh.hist)[t] = make_uint4(0, 0, 0, 0);
     lds_barrier();
 #pragma unroll
     for (int j = 0; j < KPT; ++j)
@@ -122,7 +124,7 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
     lds_barrier();
     int above = incl - local;
 #pragma unroll
-    for (int w = 0; w < kTkNW; ++w) above += w < wv ? sh.wsum[w] : 0;
+    for (int w = 0; w < NT / 64; ++w) above += w < wv ? sh.wsum[w] : 0;
     if (above < remaining && remaining <= above + local) {
 #pragma unroll
       for (int u = 15; u >= 0; --u) {
@@ -153,13 +155,15 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
 // every word the number of taken elements before it (all the keys above,
 // the first `remaining` equal ones), and each thread writes the taken
 // elements of its words.
-template <int KPT>
+template <int KPT, int NT = kTkNT>
 __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n, uint32_t prefix, uint32_t pmask,
                                               int remaining, SelShared &sh) {
+  constexpr int W = NT / 32;  // bitmap words per register slot
+  static_assert(W * KPT <= 16 * kTopkMergeKPT, "the bitmaps fit");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int nr = (n + kTkNT - 1) / kTkNT;
+  const int nr = (n + NT - 1) / NT;
   uint32_t *bg = sh.bits[0], *be = sh.bits[1];
-  // word 16 j + 2 wv + h holds the elements 512 j + 64 wv + 32 h + bit
+  // word W j + 2 wv + h holds the elements NT j + 64 wv + 32 h + bit
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     if (j < nr) {
@@ -167,16 +171,16 @@ __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n,
       const uint64_t g = __ballot(km > prefix);
       const uint64_t q = __ballot(km == prefix && key[j] != 0u);
       if (lane == 0) {
-        *reinterpret_cast<uint2 *>(&bg[16 * j + 2 * wv]) = make_uint2((uint32_t)g, (uint32_t)(g >> 32));
-        *reinterpret_cast<uint2 *>(&be[16 * j + 2 * wv]) = make_uint2((uint32_t)q, (uint32_t)(q >> 32));
+        *reinterpret_cast<uint2 *>(&bg[W * j + 2 * wv]) = make_uint2((uint32_t)g, (uint32_t)(g >> 32));
+        *reinterpret_cast<uint2 *>(&be[W * j + 2 * wv]) = make_uint2((uint32_t)q, (uint32_t)(q >> 32));
       }
     }
   }
   lds_barrier();
   // thread t takes the words t * per .. t * per + per - 1
-  const int nw = 16 * nr;
-  constexpr int kPerMax = (16 * KPT + kTkNT - 1) / kTkNT;
-  const int per = (nw + kTkNT - 1) / kTkNT;
+  const int nw = W * nr;
+  constexpr int kPerMax = (W * KPT + NT - 1) / NT;
+  const int per = (nw + NT - 1) / NT;
   uint32_t wg[kPerMax], wq[kPerMax];
   uint32_t cnt = 0u;  // above-threshold count | equal count << 16 (each total below 2^16)
 #pragma unroll
@@ -197,7 +201,7 @@ __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n,
   lds_barrier();
   uint32_t before = incl - cnt;
 #pragma unroll
-  for (int w = 0; w < kTkNW; ++w) before += w < wv ? (uint32_t)sh.wsum[w] : 0u;
+  for (int w = 0; w < NT / 64; ++w) before += w < wv ? (uint32_t)sh.wsum[w] : 0u;
   int gb = (int)(before & 0xFFFFu), qb = (int)(before >> 16);  // keys above / equal to the threshold before this thread's words
   int32_t *list = reinterpret_cast<int32_t *>(sh.hist);
 #pragma unroll
@@ -476,7 +480,8 @@ __global__ void __launch_bounds__(kTkNT) __attribute__((amdgpu_waves_per_eu(4)))
 // Merge of a segmented node: the topk of the survivors of all its segments.
 // Segment s holds k slots (survivors in index order, then padding key 0), so
 // the slots of all segments in order list the survivors in index order.
-__global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheView c, const uint64_t *__restrict__ anc,
+template <int NT>
+__global__ void __launch_bounds__(NT, 1) topk_merge_kernel(tv_dims d, CacheView c, const uint64_t *__restrict__ anc,
                                                            const int32_t *__restrict__ depth,
                                                            const uint16_t *__restrict__ scr_c4,
                                                            int32_t *__restrict__ sel,
@@ -507,19 +512,21 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   const int64_t sv = (int64_t)node * max_seg * k;
   const int cnt_s = tid < max_seg ? surv_cnt[node * max_seg + tid] : 0;  // max_seg <= 64: wave 0
   const int all_slots = max_seg * k;
-  const int nr_all = (all_slots + kTkNT - 1) / kTkNT;
-  uint32_t key[kTopkMergeKPT];
+  constexpr int KPT = kTopkMergeCap / NT;
+  static_assert(KPT * NT == kTopkMergeCap, "merge capacity");
+  const int nr_all = (all_slots + NT - 1) / NT;
+  uint32_t key[KPT];
 #pragma unroll
-  for (int j = 0; j < kTopkMergeKPT; ++j)
-    key[j] = j < nr_all ? surv_key[sv + std::min(tid + kTkNT * j, all_slots - 1)] : 0u;
+  for (int j = 0; j < KPT; ++j)
+    key[j] = j < nr_all ? surv_key[sv + std::min(tid + NT * j, all_slots - 1)] : 0u;
   if (status != TV_ROW_OK || !len_ok(L, d.max_len)) return;
   const int n4 = L / d.ratio_csa;
   const int nseg = topk_segments(n4);
   if (nseg <= 1) return;
   const int slots = nseg * k;
 #pragma unroll
-  for (int j = 0; j < kTopkMergeKPT; ++j)
-    if (tid + kTkNT * j >= slots) key[j] = 0u;
+  for (int j = 0; j < KPT; ++j)
+    if (tid + NT * j >= slots) key[j] = 0u;
   if (tid < 64) {
     int run = tid < nseg ? cnt_s : 0;
 #pragma unroll
@@ -535,11 +542,11 @@ __global__ void __launch_bounds__(kTkNT, 1) topk_merge_kernel(tv_dims d, CacheVi
   const bool all = total <= k;  // every real survivor (key above 0) is taken
   uint32_t prefix = 0u, pmask = 0xFFFFFFFFu;
   int remaining = 0;
-  if (!all) radix_threshold<kTopkMergeKPT>(key, slots, k, sh, prefix, pmask, remaining);
-  compact_taken<kTopkMergeKPT>(key, slots, prefix, pmask, remaining, sh);
+  if (!all) radix_threshold<KPT, NT>(key, slots, k, sh, prefix, pmask, remaining);
+  compact_taken<KPT, NT>(key, slots, prefix, pmask, remaining, sh);
   const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
   const int taken = all ? total : k;
-  for (int t = tid; t < k; t += kTkNT) {
+  for (int t = tid; t < k; t += NT) {
     const int s = t < taken ? surv_idx[sv + std::min(std::max(list[t], 0), slots - 1)] : -1;
     out[t] = s;
     if (s >= 0) tab[t] = csa_row(d, nk, b, s, path, c.c4, c4b, c.page_table, scr_c4);
@@ -589,7 +596,8 @@ hipError_t launch_topk_merge(const tv_dims &d, const CacheView &c, const uint64_
                              hipStream_t s) {
   const int max_seg = topk_max_segments(d);
   if (max_seg <= 1) return hipSuccess;
-  topk_merge_kernel<<<(unsigned)((int64_t)d.B * d.D), kTkNT, 0, s>>>(d, c, anc, depth, scr_c4, sel, row_status,
+  topk_merge_kernel<kMergeNT><<<(unsigned)((int64_t)d.B * d.D), kMergeNT, 0, s>>>(d, c, anc, depth, scr_c4, sel,
+                                                                                 row_status,
                                                                      row_rank, keytab, keytab_stride, max_seg,
                                                                      surv_idx, surv_key, surv_cnt);
   return hipGetLastError();
