@@ -374,6 +374,22 @@ static tv_status layer_step(const tv_dims *d, const tv_round &r, const tv_layer 
                      split ? L.scr_c128 : nullptr);
 }
 
+static tv_status commit_check(const tv_dims *dims, const tv_cache *cache, const uint16_t *tree_u,
+                              const uint64_t *anc, const int32_t *depth, const uint16_t *scr_c4,
+                              const uint16_t *scr_c128, const int32_t *accepted_last, const int32_t *accept_nodes,
+                              const int32_t *accept_len, const int32_t *row_status, const int32_t *primary_last) {
+  tv_status st = check_dims(dims);
+  if (st != TV_OK) return st;
+  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
+      !accept_nodes || !accept_len || !row_status)
+    return TV_ERR_INVALID_ARG;
+  if (!cache_a16(cache) ||
+      !all_a16(tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes, accept_len, row_status) ||
+      (primary_last && !a16(primary_last)))
+    return TV_ERR_INVALID_ARG;
+  return check_device();
+}
+
 static tv_status layer_check(const tv_dims *d, const tv_round &r, const tv_layer &L) {
   tv_status st = compress_check(d, &L.cache, L.tree_u, r.anc, r.depth, L.gate_w, L.scr_c4, L.scr_c128, r.row_status,
                                 r.primary_last);
@@ -460,16 +476,9 @@ tv_status tv_commit_accepted_path(const tv_dims *dims, tv_cache *cache, const ui
                                   const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                                   const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
                                   int32_t *row_status, const int32_t *primary_last, hipStream_t stream) {
-  tv_status st = check_dims(dims);
+  const tv_status st = commit_check(dims, cache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes,
+                                    accept_len, row_status, primary_last);
   if (st != TV_OK) return st;
-  if (!cache_complete(*dims, cache) || !tree_u || !anc || !depth || !scr_c4 || !scr_c128 || !accepted_last ||
-      !accept_nodes || !accept_len || !row_status)
-    return TV_ERR_INVALID_ARG;
-  if (!cache_a16(cache) ||
-      !all_a16(tree_u, anc, depth, scr_c4, scr_c128, accepted_last, accept_nodes, accept_len, row_status) ||
-      (primary_last && !a16(primary_last)))
-    return TV_ERR_INVALID_ARG;
-  if ((st = check_device()) != TV_OK) return st;
   TV_LAUNCH("commit_path", launch_commit(*dims, *cache, tree_u, anc, depth, scr_c4, scr_c128, accepted_last,
                                          accept_nodes, accept_len, row_status, primary_last, stream));
   return TV_OK;
@@ -526,10 +535,20 @@ static tv_status record_round(const tv_dims *d, const tv_round &r, const tv_laye
     st = tv_select_accepted_path(d, r.parents, r.anc, r.depth, r.draft_tokens, r.target_logits, r.vocab,
                                  r.target_tokens, r.accepted_last, r.next_token, r.row_status, r.select_workspace,
                                  r.select_workspace_bytes, s);
-  for (int l = 0; l < n && st == TV_OK; ++l) {
-    tv_cache c = layers[l].cache;
-    st = tv_commit_accepted_path(d, &c, layers[l].tree_u, r.anc, r.depth, layers[l].scr_c4, layers[l].scr_c128,
-                                 r.accepted_last, r.accept_nodes, r.accept_len, r.row_status, r.primary_last, s);
+  // the commits: one launch per group of up to kCommitMaxLayers layers, each row walking its layers in order
+  for (int l0 = 0; l0 < n && st == TV_OK; l0 += kCommitMaxLayers) {
+    CommitLayers ls{};
+    ls.n = std::min(n - l0, kCommitMaxLayers);
+    for (int k = 0; k < ls.n && st == TV_OK; ++k) {
+      const tv_layer &L = layers[l0 + k];
+      st = commit_check(d, &L.cache, L.tree_u, r.anc, r.depth, L.scr_c4, L.scr_c128, r.accepted_last,
+                        r.accept_nodes, r.accept_len, r.row_status, r.primary_last);
+      ls.l[k] = CommitLayer{L.cache, L.tree_u, L.scr_c4, L.scr_c128};
+    }
+    if (st != TV_OK) break;
+    hipStream_t stream = s;
+    TV_LAUNCH("commit_path", launch_commit_layers(*d, ls, r.anc, r.depth, r.accepted_last, r.accept_nodes,
+                                                  r.accept_len, r.row_status, r.primary_last, stream));
   }
   return st;
 }

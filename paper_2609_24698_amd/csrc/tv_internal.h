@@ -124,6 +124,20 @@ hipError_t launch_attn_mla(const tv_dims &d, const uint16_t *q, const int32_t *r
                            float *part_ml, uint16_t *out, float *lse, hipStream_t s);
 hipError_t launch_combine(const tv_dims &d, const int32_t *row_status, const int32_t *nkeys, const SplitPlan &plan,
                           const float *part_o, const float *part_ml, uint16_t *out, float *lse, hipStream_t s);
+// Per-layer buffers of a multi-layer commit (kernel arguments: at most
+// kCommitMaxLayers layers per launch).
+struct CommitLayer {
+  tv_cache cache;
+  const uint16_t *tree_u, *scr_c4, *scr_c128;
+};
+constexpr int kCommitMaxLayers = 32;
+struct CommitLayers {
+  CommitLayer l[kCommitMaxLayers];
+  int32_t n;
+};
+hipError_t launch_commit_layers(const tv_dims &d, const CommitLayers &ls, const uint64_t *anc, const int32_t *depth,
+                                const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,
+                                int32_t *row_status, const int32_t *primary_last, hipStream_t s);
 hipError_t launch_commit(const tv_dims &d, const tv_cache &c, const uint16_t *tree_u, const uint64_t *anc,
                          const int32_t *depth, const uint16_t *scr_c4, const uint16_t *scr_c128,
                          const int32_t *accepted_last, int32_t *accept_nodes, int32_t *accept_len,

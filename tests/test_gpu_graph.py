@@ -63,7 +63,7 @@ def test_graph_equals_eager(name, n, select, over):
     _, rb = _layers(name, n, select, **over)
     eager, graph = LayeredRound(ra), LayeredRound(rb)
     kernels = graph.capture()
-    assert kernels >= 3 * n + n  # per layer: mask or not, compression and scoring; top-k; attention; then commits
+    assert kernels >= 3 * n + 1  # per layer: mask or not, compression and scoring; top-k; attention; then the commits
     noise = torch.empty(1 << 20, device="cuda:0")
     for rnd in range(3):
         eager.eager(fused=False)
@@ -128,6 +128,35 @@ def test_device_round_step_equals_calls():
         torch.cuda.synchronize()
         for k in keys:
             assert np.array_equal(ra[0].host(k).view(np.uint8), rb[0].host(k).view(np.uint8)), (rnd, k)
+
+
+def test_commit_failure_in_a_middle_layer():
+    """A row whose layer-1 pool has no slot for the accepted path's new CSA
+    entry: layer 0 commits it, layer 1 fails it (TV_ROW_CAPACITY), layer 2
+    skips it; the graph's one-launch commit of all layers equals the calls
+    issued layer by layer, bit for bit."""
+    from paper_2609_24698_amd import LayeredRound
+    ws, ra = _layers("C1", 3, False, lens=8191)  # every root closes a CSA block
+    _, rb = _layers("C1", 3, False, lens=8191)
+    w = ws[0]
+    _, depth, _ = O.build_tree_mask(w.parents)
+    rows = [b for b in range(w.B)
+            if any((int(w.lens[b]) + t + 1) % 4 == 0 for t in range(int(depth[b, w.accepted_last[b]]) + 1))]
+    assert rows, "no row whose accepted path closes a CSA block"
+    row = rows[0]
+    for r in (ra[1], rb[1]):
+        r.t["c4_cap"][row] = int(w.lens[row]) // 4  # room for the committed entries only
+    eager, graph = LayeredRound(ra), LayeredRound(rb)
+    graph.capture()
+    eager.eager(fused=False)
+    graph.replay()
+    torch.cuda.synchronize()
+    _same(eager, graph, 0)
+    assert int(rb[0].host("row_status")[row]) == O.ROW_CAPACITY
+    assert int(rb[0].host("len")[row]) > int(w.lens[row])    # layer 0 committed
+    assert int(rb[1].host("len")[row]) == int(w.lens[row])   # layer 1 failed
+    assert int(rb[2].host("len")[row]) == int(w.lens[row])   # layer 2 skipped
+    graph.release()
 
 
 def test_new_trees_without_recapture():
