@@ -9,9 +9,10 @@
 // One workgroup per row.  All checks run before the first write, so a failing
 // row is left exactly as it was.  Destinations follow the cache layout: the
 // ring and per-row pools, or with a paged pool the raw, CSA and HCA layers
-// through the row's page table (a page it does not allocate fails the row).  The row's loads go out together; the copies
-// (ring rows, CSA and HCA entries) form one list of 16-byte chunks whose
-// loads a thread issues before its stores.
+// through the row's page table (a page it does not allocate fails the row).
+// The row's loads go out together; the copies (ring rows, CSA and HCA
+// entries) form one list of 16-byte chunks whose loads a thread issues
+// before its stores.
 //
 // With FP8 indexer keys a CSA entry's indexer channels (E4M3 values held
 // in bfloat16 in scratch) are narrowed, exactly, to E4M3 codes in the pool.

@@ -24,8 +24,10 @@ __device__ __forceinline__ float dot8(const float *g, uint4 v) {
          g[4] * bf2f_lo(v.z) + g[5] * bf2f_hi(v.z) + g[6] * bf2f_lo(v.w) + g[7] * bf2f_hi(v.w);
 }
 
-// The short-block path (wavefront 0 only; see above).  q0 is the block's
-// first position, m the node's ancestor mask, dj the depth of node `lane`.
+// The short-block path, run by one wavefront per node (see above); it uses
+// no workgroup barrier.  q0 is the block's first position, R its token count,
+// m the node's ancestor mask, dj the depth of node `lane`, path an LDS array
+// of the wavefront's own.
 __device__ void compress_short(const tv_dims &d, const CacheView &c, const uint16_t *__restrict__ tree_u,
                                const uint16_t *__restrict__ gate_w, int b, int64_t node, int32_t L, int64_t q0, int R,
                                uint64_t m, int32_t dj, int32_t *path, uint16_t *__restrict__ scr_c4,

@@ -7,7 +7,8 @@
 // branch (Sec. 3.1, Sec. 4.1).
 //
 // Selection is an exact radix select on order-preserving 32-bit keys held in
-// registers (element e of a workgroup in slot e / 512 of thread e % 512):
+// registers (element e of an NT-thread workgroup in slot e / NT of thread
+// e % NT; NT is 512 for a segment and 1024 for a merge):
 // 13-bit digits counted in an LDS histogram, each pass restricted to the keys
 // that share the digits found so far, until the bin holding the topk-th key
 // holds exactly the keys still needed or every bit is fixed.  An ordered
@@ -65,7 +66,7 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b) {
 }
 
 // Threshold of the k largest of the keys the workgroup holds (key[j] is
-// element tid + 512 j; elements from n on, and any other padding, hold key 0,
+// element tid + NT j; elements from n on, and any other padding, hold key 0,
 // below every real key, and are never counted or taken; k < the number of
 // real keys).  On return
 // every thread has prefix, pmask and remaining such that the k largest are the
