@@ -1,11 +1,12 @@
 """Benchmark of one verify round per step on one MI355X.
 
 A step is the whole hot path over one batch: tree mask, per-branch
-compression and verify attention in one library call (the mask and the
-indexer scoring share a launch), then the accepted-path commit, for B rows of
-D-node draft trees.  Every step commits its accepted path, so the committed context
-grows by the accepted length (at most D tokens per row per step) like a
-decoding loop would.  Inputs are synthetic and already resident in HBM.
+compression and verify attention in one library call (the mask, the CSA
+entries and the indexer scoring share a launch; the HCA entries share the
+top-k's), then the accepted-path commit, for B rows of D-node draft trees.
+Every step commits its accepted path, so the committed context grows by the
+accepted length (at most D tokens per row per step) like a decoding loop
+would.  Inputs are synthetic and already resident in HBM.
 
 Cold and warm caches.  Between two verify rounds of one layer a decoder runs
 every other layer of the model, so a layer's KV is no longer in the 256 MB

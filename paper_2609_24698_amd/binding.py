@@ -339,9 +339,9 @@ class DeviceRound:
                                     t["row_status"], stream)
 
     def verify_round(self, stream=None, with_mask: bool = True):
-        """mask + compress + verify in one library call (tv_verify_round):
-        the indexer scoring runs beside the compression.  ``with_mask=False``
-        reuses the masks already in anc/depth."""
+        """mask + compress + verify in one library call (tv_verify_round),
+        bit-identical to the three calls with fewer launches.
+        ``with_mask=False`` reuses the masks already in anc/depth."""
         t = self.t
         rnd = round_struct(t, t["parents"] if with_mask else None, getattr(self, "vocab", 0))
         layer = layer_struct(self.cache, t)

@@ -3,8 +3,8 @@ same calls issued one by one, round after round (the committed state grows),
 with eager work and synchronisations between replays, and with new draft
 trees written into the captured buffers between replays.  Layer 0 of the
 first round is also checked against the oracle.  The one-call layer step
-(tv_verify_round, indexer scoring beside the compression on a second
-stream) gives the same bits as the separate calls on one stream."""
+(tv_verify_round: mask, compression and indexer scoring sharing launches)
+gives the same bits as the separate calls."""
 import sys
 
 import numpy as np

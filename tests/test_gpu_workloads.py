@@ -179,7 +179,7 @@ def test_softmax_restart(config):
     _say(f"  restart case: {stats}")
 
 
-def test_mla_stream_of_many_units():
+def test_mla_many_units():
     """72 rows of the shared-latent shape (576 node units, more than two per
     compute unit), lengths from a few hundred to a few thousand, and in every
     third row a committed window key whose logits exceed the first tile's
@@ -195,7 +195,7 @@ def test_mla_stream_of_many_units():
         w.ring[b, (L - 1) % cap] = O.f64_to_bf16(row)
     rows = [0, 1, 3, 35, 69, 70, int(np.argmax(w.lens)), int(np.argmin(w.lens))]
     nodes = [(b, i) for b in sorted(set(rows)) for i in range(w.D)]
-    _say(f"[workload] C1 shape B=72 stream rows={sorted(set(rows))}")
+    _say(f"[workload] C1 shape B=72 rows={sorted(set(rows))}")
     ref = O.run_round(w, nodes)
     stats = _check_stages(w, ref, _device(w), nodes, rerun=_rerun(w, ref))
     _say(f"  {stats}")
