@@ -15,6 +15,7 @@ import synth
 from oracle import tv_oracle as O
 
 from .parity import compare_verify
+from .test_gpu_parity import SMALL_CASES
 
 pytestmark = pytest.mark.gpu
 
@@ -112,6 +113,30 @@ def test_one_call_layer_step_equals_calls(name, n, select, over):
         torch.cuda.synchronize()
         _same(calls, fused, rnd)
     assert np.all(rb[0].host("row_status") == 0)
+
+
+@pytest.mark.parametrize("case", SMALL_CASES, ids=lambda c: "-".join(f"{k}{v}" for k, v in c.items() if k != "name")
+                         or "base")
+def test_one_call_small_cases(case):
+    """The one-call layer step on the small parity cases (empty and short
+    rows, lengths at block boundaries, D from 1 to 64, chains, both head
+    shapes, the long-block compression, FP8 keys, paged pools): verify_round
+    then commit against mask, compress, verify and commit, every output and
+    the cache bit for bit, two rounds in a row."""
+    from paper_2609_24698_amd import DeviceRound
+    c = dict(case)
+    name = c.pop("name")
+    c.setdefault("max_len_margin", 64)
+    _say(f"[one-call small] {name} {c}")
+    ra = DeviceRound(synth.make_workload(name, **c), "cuda:0")
+    rb = DeviceRound(synth.make_workload(name, **c), "cuda:0")
+    keys = [k for k in PER_LAYER + SHARED if k in ra.t]
+    for rnd in range(2):
+        ra.round_calls()
+        rb.round()
+        torch.cuda.synchronize()
+        for k in keys:
+            assert np.array_equal(ra.host(k).view(np.uint8), rb.host(k).view(np.uint8)), (rnd, k)
 
 
 def test_device_round_step_equals_calls():
