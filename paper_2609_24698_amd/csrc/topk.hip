@@ -115,12 +115,7 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
     int local = 0;
 #pragma unroll
     for (int u = 0; u < 16; ++u) local += (int)h[u];
-    int incl = local;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += y;
-    }
+    const int incl = (int)wave_prefix_sum((uint32_t)local);
     if (lane == 63) sh.wsum[wv] = incl;
     lds_barrier();
     int above = incl - local;
@@ -192,12 +187,7 @@ __device__ __forceinline__ void compact_taken(const uint32_t (&key)[KPT], int n,
     wq[u] = ok ? be[w] : 0u;
     cnt += (uint32_t)__popc(wg[u]) | ((uint32_t)__popc(wq[u]) << 16);
   }
-  uint32_t incl = cnt;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = (uint32_t)__shfl_up((int)incl, o, 64);
-    if (lane >= o) incl += y;
-  }
+  const uint32_t incl = wave_prefix_sum(cnt);
   if (lane == 63) sh.wsum[wv] = (int)incl;
   lds_barrier();
   uint32_t before = incl - cnt;
@@ -307,8 +297,7 @@ __device__ __forceinline__ void topk_node(const tv_dims &d, const CacheView &c, 
     const int32_t Lr = c.len[r];
     nb += (Lr > L || (Lr == L && r < b)) ? 1 : 0;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) nb += __shfl_xor(nb, o, 64);
+  nb = (int)wave_total((uint32_t)nb);
   if (lane == 0) wcnt[wv] = nb;
   auto rank_of_row = [&]() {  // after a barrier
     int rk = 0;
@@ -529,9 +518,7 @@ __global__ void __launch_bounds__(NT, 1) topk_merge_kernel(tv_dims d, CacheView 
   for (int j = 0; j < KPT; ++j)
     if (tid + NT * j >= slots) key[j] = 0u;
   if (tid < 64) {
-    int run = tid < nseg ? cnt_s : 0;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) run += __shfl_xor(run, o, 64);
+    const int run = (int)wave_total(tid < nseg ? (uint32_t)cnt_s : 0u);
     if (tid == 0) real_cnt = run;
   }
   uint64_t csa_mask;

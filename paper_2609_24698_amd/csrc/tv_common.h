@@ -84,6 +84,24 @@ __device__ __forceinline__ const uint16_t *ring_row(const uint16_t *ring, int b,
   return ring + ((int64_t)b * ring_cap + (q & (ring_cap - 1))) * d_u;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront (lane l gets the
+// sum over lanes 0..l), from DPP row shifts (a Hillis-Steele scan inside
+// each 16-lane row) and two row broadcasts: no LDS-crossbar shuffles.  Every
+// lane of the wavefront must be active.
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
+  return x;
+}
+// Sum over the wavefront's 64 lanes, the same value in every lane.
+__device__ __forceinline__ uint32_t wave_total(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_prefix_sum(x), 63);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
