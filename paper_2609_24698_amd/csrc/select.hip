@@ -122,8 +122,7 @@ __global__ void __launch_bounds__(kSelNT) argmax_kernel(const uint16_t *__restri
       if (any_nan ? (hi != hi) : (hi == M)) idx = e + 1 < vocab ? e + 1 : idx;
       if (any_nan ? (lo != lo) : (lo == M)) idx = e < vocab ? e : idx;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) idx = min(idx, __shfl_xor(idx, o, 64));
+    idx = wave_min_i32(idx);  // the wavefront's condition is uniform: every lane is here
   }
   if (lane == 0) red_idx[wv] = idx;
   __syncthreads();
@@ -167,8 +166,7 @@ __global__ void __launch_bounds__(256) select_kernel(int B, int D, int chunks, c
   // accepted: every non-root node of the root path (bits of anc) matches
   const bool ok = live && (i == 0 || ((m & ~1ull & ~M) == 0));
   uint32_t key = ok ? (uint32_t(dep) << 8) | uint32_t(255 - i) : 0u;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) key = max(key, (uint32_t)__shfl_xor((int)key, o, 64));
+  key = wave_max_u32(key);
   const int last = 255 - int(key & 255u);
   const int32_t t_last = __shfl(t, last, 64);
   if (lane == 0) {
