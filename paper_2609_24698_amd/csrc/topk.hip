@@ -67,16 +67,21 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b) {
 
 // Threshold of the k largest of the keys the workgroup holds (key[j] is
 // element tid + NT j; elements from n on, and any other padding, hold key 0,
-// below every real key, and are never counted or taken; k < the number of
-// real keys).  On return
+// below every real key, and are never counted or taken; n_real keys are
+// real, all of them below element n, and k < n_real).  On return
 // every thread has prefix, pmask and remaining such that the k largest are the
 // keys with (key & pmask) > prefix and the `remaining` lowest elements with
 // (key & pmask) == prefix.
 template <int KPT, int NT = kTkNT>
-__device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int n, int k, SelShared &sh,
-                                                uint32_t &prefix, uint32_t &pmask, int &remaining) {
+__device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int n, int n_real, int k,
+                                                SelShared &sh, uint32_t &prefix, uint32_t &pmask,
+                                                int &remaining) {
   static_assert(NT % 64 == 0 && NT / 64 <= 16 && 16 * NT >= kTkBins, "wave sums and the scan's bins fit");
   const int nr = (n + NT - 1) / NT;  // slots that hold any element below n
+  // Padding keys (0) match the prefix only while it is 0, and then all fall
+  // into bin 0: that bin starts at minus their count instead of each key
+  // being tested (a test the compiler would keep as one mask per slot).
+  const uint32_t n_pad = (uint32_t)(nr * NT - n_real);
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   prefix = 0;
   pmask = 0;
@@ -88,11 +93,16 @@ __device__ __forceinline__ void radix_threshold(const uint32_t (&key)[KPT], int 
     const int sft = shift - nb;
     const int nbins = 1 << nb;
     const uint32_t dmask = (uint32_t)nbins - 1u;
-    for (int t = tid; t < nbins / 4; t += NT) reinterpret_cast<uint4 *>(sh.hist)[t] = make_uint4(0, 0, 0, 0);
+    for (int t = tid; t < nbins / 4; t += NT)
+      reinterpret_cast<uint4 *>(sh.hist)[t] = make_uint4(t == 0 && prefix == 0u ? 0u - n_pad : 0u, 0u, 0u, 0u);
     lds_barrier();
+    // The slot bound, laundered through a scalar move each pass: a bound known
+    // across passes becomes one lane mask per slot, kept for every pass.
+    int nr_p;
+    asm volatile("s_mov_b32 %0, %1" : "=s"(nr_p) : "s"(nr));
 #pragma unroll
     for (int j = 0; j < KPT; ++j)
-      if (j < nr && key[j] != 0u && (key[j] & pmask) == prefix) atomicAdd(&sh.hist[(key[j] >> sft) & dmask], 1u);
+      if (j < nr_p && (key[j] & pmask) == prefix) atomicAdd(&sh.hist[(key[j] >> sft) & dmask], 1u);
     lds_barrier();
     // Thread t owns the 16 bins from nbins - 16 (t + 1) up (threads 0.. hold
     // the top bins), read as four 16-byte groups; counts scan from the top.
@@ -400,7 +410,7 @@ __device__ __forceinline__ void topk_node(const tv_dims &d, const CacheView &c, 
   if (!all) {
     uint32_t prefix, pmask;
     int remaining;
-    radix_threshold<kTkKPT>(key, seg_n, k, sh, prefix, pmask, remaining);
+    radix_threshold<kTkKPT>(key, seg_n, seg_n, k, sh, prefix, pmask, remaining);
     compact_taken<kTkKPT>(key, seg_n, prefix, pmask, remaining, sh);
   }
   const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
@@ -530,7 +540,7 @@ __global__ void __launch_bounds__(NT, 1) topk_merge_kernel(tv_dims d, CacheView 
   const bool all = total <= k;  // every real survivor (key above 0) is taken
   uint32_t prefix = 0u, pmask = 0xFFFFFFFFu;
   int remaining = 0;
-  if (!all) radix_threshold<KPT, NT>(key, slots, k, sh, prefix, pmask, remaining);
+  if (!all) radix_threshold<KPT, NT>(key, slots, total, k, sh, prefix, pmask, remaining);
   compact_taken<KPT, NT>(key, slots, prefix, pmask, remaining, sh);
   const int32_t *list = reinterpret_cast<const int32_t *>(sh.hist);
   const int taken = all ? total : k;
