@@ -86,18 +86,30 @@ def attention_bytes(dims, lens, sel, depth, anc):
     """Algorithmic HBM bytes of one verify-attention launch.
 
     Queries, outputs (bf16) and lse; the selection lists; the union over the
-    row's nodes of the CSA rows they select (each row once); every HCA entry a
-    node of the row sees; the committed window rows of the row (the root's
-    window is the widest); the row's draft-token rows.
+    row's nodes of the CSA rows they select (each row once: a committed entry
+    by its index, an entry closed on a path by the scratch slot of the node
+    that closed it, since siblings close the same index in different slots);
+    every HCA entry a node of the row sees; the committed window rows of the
+    row (the root's window is the widest); the row's draft-token rows.
     """
     B, D, H = dims["B"], dims["D"], dims["H"]
+    r4 = dims["ratio_csa"]
     row = dims["d_row"] * 2
     total = B * D * H * (dims["d_k"] * 2 + dims["d_v"] * 2 + 4)
     total += B * D * dims["topk"] * 4
     for b in range(B):
         L = int(lens[b])
-        s = sel[b]
-        total += len(np.unique(s[s >= 0])) * row
+        n4 = L // r4
+        committed, closers = set(), set()
+        for i in range(D):
+            si = sel[b, i][sel[b, i] >= 0]
+            committed.update(int(x) for x in si[si < n4])
+            on_path = set(int(x) for x in si[si >= n4])
+            for j in range(D):
+                q = L + int(depth[b, j]) + 1
+                if (int(anc[b, i]) >> j) & 1 and q % r4 == 0 and q // r4 - 1 in on_path:
+                    closers.add(j)
+        total += (len(committed) + len(closers)) * row
         total += (L // dims["ratio_hca"]) * row
         hca_closers = {j for j in range(D) if (L + int(depth[b, j]) + 1) % dims["ratio_hca"] == 0}
         total += len(hca_closers) * row

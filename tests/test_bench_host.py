@@ -38,3 +38,47 @@ def test_layout_check_rejects_bad_padding():
         sel[b, i, [0, 1]] = sel[b, i, [1, 0]]  # not ascending
     with pytest.raises(AssertionError):
         bench.check_selection_layout(w.dims, w.lens, ref["depth"], ref["anc"], sel)
+
+
+def _distinct_rows(w, ref):
+    """Every stored row the attention reads, by identity, from the oracle's key
+    sets: committed CSA entries by index, path CSA entries by the scratch slot
+    (closing node) they come from, committed and path HCA entries, committed
+    window rows by position, draft rows by node."""
+    d = w.dims
+    r4, r128, W = d["ratio_csa"], d["ratio_hca"], d["window"]
+    rows = set()
+    for (b, i), det in ref["detail"].items():
+        L = int(w.lens[b])
+        n4 = L // r4
+        path = O.node_path(ref["anc"][b], ref["depth"][b], i)
+        closer = {(L + int(ref["depth"][b, j]) + 1) // r4 - 1: j for j in path
+                  if (L + int(ref["depth"][b, j]) + 1) % r4 == 0}
+        for s in det["sel"].tolist():
+            rows.add((b, "c4", s) if s < n4 else (b, "scr4", closer[s]))
+        rows.update((b, "c128", s) for s in range(L // r128))
+        rows.update((b, "scr128", j) for j in path if (L + int(ref["depth"][b, j]) + 1) % r128 == 0)
+        p = L + int(ref["depth"][b, i])
+        rows.update((b, "ring", q) for q in range(max(0, p - W + 1), L))
+        rows.update((b, "tree", j) for j in path)
+    return rows
+
+
+@pytest.mark.parametrize("case", [
+    dict(name="C0", B=3, D=8, tree="random", lens=[381, 3967, 1023], seed=33, topk=16),
+    dict(name="C1", B=2, D=8, lens=[1000, 3001], seed=40, topk=64),
+    dict(name="C1", B=2, D=8, tree=[-1, 0, 0, 1, 2, 1, 2, 3], lens=[8190, 1021], seed=52, topk=64),
+    # take-all: nodes 1 and 2 (siblings at depth 1) both close block 63, and every node below each selects it
+    dict(name="C1", B=2, D=8, tree=[-1, 0, 0, 1, 2, 1, 2, 3], lens=[254, 510], seed=53, topk=256),
+])
+def test_attention_bytes_count_each_stored_row_once(case):
+    """The roofline's algorithmic bytes: queries, outputs, lse and selections,
+    plus every distinct stored row the oracle's key sets read, each once (a
+    sibling pair closing the same block reads two scratch rows)."""
+    c = dict(case)
+    w = synth.make_workload(c.pop("name"), **c)
+    ref = O.run_round(w)
+    d = w.dims
+    fixed = d["B"] * d["D"] * (d["H"] * (d["d_k"] * 2 + d["d_v"] * 2 + 4) + d["topk"] * 4)
+    want = fixed + len(_distinct_rows(w, ref)) * d["d_row"] * 2
+    assert bench.attention_bytes(d, w.lens, ref["sel"], ref["depth"], ref["anc"]) == want
