@@ -56,6 +56,7 @@ def _same(a, b, rnd):
     ("C1", 3, True, {}),
     ("C0", 4, False, dict(lens=2047)),
     ("C2", 2, True, dict(B=4, lens=[32767, 20000, 4099, 1023])),
+    ("C0", 33, False, dict(B=3, D=8, tree="random", lens=[2047, 1023, 3071], topk=16)),  # two commit launches
 ])
 def test_graph_equals_eager(name, n, select, over):
     from paper_2609_24698_amd import LayeredRound
