@@ -59,3 +59,32 @@ def test_random_configuration(k):
         torch.cuda.synchronize()
         for key in keys:
             assert np.array_equal(ra.host(key).view(np.uint8), rb.host(key).view(np.uint8)), (rnd, key)
+
+
+@pytest.mark.parametrize("k", range(8))
+def test_random_graph_round(k):
+    """The captured multi-layer round on random configurations: every replay
+    equals the same calls issued one by one, three rounds, with the
+    program's own eager work between replays."""
+    from paper_2609_24698_amd import LayeredRound
+    from .test_gpu_graph import _layers, _same
+    c = random_config(100 + k)
+    name = c.pop("name")
+    c.pop("seed")
+    c.pop("max_len_margin")
+    n = 2 + k % 2
+    select = k % 3 == 0
+    print(f"[random graph {k}] {name} layers={n} select={select} {c}", flush=True)
+    _, ra = _layers(name, n, select, **c)
+    _, rb = _layers(name, n, select, **c)
+    eager, graph = LayeredRound(ra), LayeredRound(rb)
+    graph.capture()
+    noise = torch.empty(1 << 20, device="cuda:0")
+    for rnd in range(3):
+        eager.eager(fused=False)
+        graph.replay()
+        torch.cuda.synchronize()
+        _same(eager, graph, rnd)
+        noise.normal_()
+        torch.cuda.synchronize()
+    graph.release()
