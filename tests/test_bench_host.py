@@ -82,3 +82,16 @@ def test_attention_bytes_count_each_stored_row_once(case):
     fixed = d["B"] * d["D"] * (d["H"] * (d["d_k"] * 2 + d["d_v"] * 2 + 4) + d["topk"] * 4)
     want = fixed + len(_distinct_rows(w, ref)) * d["d_row"] * 2
     assert bench.attention_bytes(d, w.lens, ref["sel"], ref["depth"], ref["anc"]) == want
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """`bench.py --gpus N` with N above 1 exits with a message before it touches a GPU."""
+    import json
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    p = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert p.returncode == 2
+    assert "one GPU" in json.loads(p.stdout.strip().splitlines()[-1])["error"]
