@@ -20,8 +20,9 @@
 // probabilities of tile it+1 and the P V of tile it.  K tiles live in four
 // LDS buffers (tile u in buffer u % 4), stored group-major: column group g
 // (64 channels, 128 bytes) of all 32 rows, then group g+1, the 16-byte chunk
-// slot XOR-swizzled by row pair, so that the logit reads (32 rows x one chunk)
-// and the transpose reads are free of bank conflicts.
+// slot XOR-swizzled per row (slot()) so that both the logit reads (32 rows x
+// one chunk, 16-byte reads) and the value transpose reads (8 rows x four
+// chunks) are free of bank conflicts.
 //
 // The probabilities use a fixed reference per head (the first tile's
 // maximum), so the output accumulators are never rescaled; if any logit of
@@ -54,7 +55,13 @@ static_assert(kDV == 128 * 4, "four value waves of 128 channels");
 static_assert(kGroups == 9, "eight value groups and one rope group");
 
 // 16-byte chunk slot of logical chunk `c` (0..7 within its group) in row r.
-__device__ constexpr int slot(int r, int c) { return c ^ ((r >> 1) & 7); }
+// Measured with the LDS bank-conflict counter on gfx950: a 16-byte read
+// conflicts unless rows of one parity within 16 rows take distinct XOR
+// values, and the 8-byte transpose read conflicts unless rows r and r + 2
+// of each group of four fall in different 64-byte halves (bit 2).  The XOR
+// (bit 1 of r into bit 2, bits 2-3 of r into bits 0-1) meets both; XOR by
+// the row pair alone left the transpose reads 2-way conflicted.
+__device__ constexpr int slot(int r, int c) { return c ^ ((((r >> 1) & 1) << 2) | ((r >> 2) & 3)); }
 // Byte offset in a tile of channel `col` of row r.
 __device__ constexpr int off(int r, int col) {
   return (col >> 6) * kGB + r * 128 + slot(r, (col >> 3) & 7) * 16 + (col & 7) * 2;
