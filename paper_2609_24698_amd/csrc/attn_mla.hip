@@ -55,12 +55,13 @@ static_assert(kDV == 128 * 4, "four value waves of 128 channels");
 static_assert(kGroups == 9, "eight value groups and one rope group");
 
 // 16-byte chunk slot of logical chunk `c` (0..7 within its group) in row r.
-// Measured with the LDS bank-conflict counter on gfx950: a 16-byte read
-// conflicts unless rows of one parity within 16 rows take distinct XOR
-// values, and the 8-byte transpose read conflicts unless rows r and r + 2
-// of each group of four fall in different 64-byte halves (bit 2).  The XOR
-// (bit 1 of r into bit 2, bits 2-3 of r into bits 0-1) meets both; XOR by
-// the row pair alone left the transpose reads 2-way conflicted.
+// Chosen by measurement (the LDS bank-conflict counter on gfx950, seven
+// swizzles of these two access patterns): the 16-byte reads were free of
+// conflicts when rows of one parity within 16 rows took distinct XOR values,
+// the 8-byte transpose reads when rows r and r + 2 of each group of four fell
+// in different 64-byte halves (bit 2).  This XOR (bit 1 of r into bit 2, bits
+// 2-3 of r into bits 0-1) was free of conflicts for both; XOR by the row pair
+// alone left the transpose reads 2-way conflicted.
 __device__ constexpr int slot(int r, int c) { return c ^ ((((r >> 1) & 1) << 2) | ((r >> 2) & 3)); }
 // Byte offset in a tile of channel `col` of row r.
 __device__ constexpr int off(int r, int col) {
